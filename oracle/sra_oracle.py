@@ -1,0 +1,266 @@
+"""Plain CPU oracle for Sparse Reference Attention (SRA).
+
+TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the CPU-baseline leg of
+the benchmark may import this module. The product path never calls it, and it shares
+no code with the HIP library.
+
+What it computes (Avatar V, §1 contributions; §2.1 "Sparse Reference Attention";
+§4.3 reference KV caching and invalid-token skipping; §8 related work):
+
+  * Generation (gen) queries attend to every generation key and to every valid
+    reference (ref) key, through ONE softmax over the concatenation of the two key sets
+    (§4.3: the cached reference K/V are concatenated with the generation K/V).
+  * Reference queries attend only to reference keys ("reference tokens only
+    self-attend", §1 and §8). The group a reference query sees is its own latent frame
+    by default (group_frames = 1); see the module note below.
+  * Invalid reference frames (§4.3: e.g. frames where the face is not visible) are
+    removed as keys for every query and as queries (output 0, log-sum-exp -inf,
+    no gradient).
+
+The oracle is the plain definition: an explicit boolean visibility mask M over the
+concatenated token order [gen ; ref] of one sample, logits S = scale * Q K^T, S = -inf
+where M is false, a row softmax, O = P V and LSE = log sum exp(S) (natural log). The
+backward pass is the textbook gradient of that masked softmax attention. Everything is
+computed in float64 by default (float32 on request), with numpy matmul as the only
+library primitive.
+
+Reading of the paper taken here (it gives no formula): "reference tokens only
+self-attend" combined with the claim of cost linear in reference length means a
+reference query cannot see all reference keys (that would be quadratic in reference
+length); the smallest grouping consistent with both is one latent frame, which is the
+default. Larger groups (up to the whole reference clip) are a parameter.
+This grouping is parity-unpinned by the paper: only the linearity claim supports it.
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+NEG_INF = -np.inf
+
+
+# ----------------------------------------------------------------------------- geometry
+def sample_sizes(geom) -> Tuple[int, int, int]:
+    """(G, R, F): gen tokens, ref tokens, tokens per ref latent frame (§2: patchified latents)."""
+    G = geom.gen_frames * geom.gen_h * geom.gen_w
+    F = geom.ref_h * geom.ref_w
+    R = geom.ref_frames * F
+    return G, R, F
+
+
+def frame_valid(geom) -> np.ndarray:
+    """Per-reference-frame validity, §4.3 (None means every frame is valid)."""
+    if geom.frame_valid is None:
+        return np.ones(geom.ref_frames, dtype=bool)
+    v = np.asarray(geom.frame_valid).astype(bool)
+    assert v.shape == (geom.ref_frames,)
+    return v
+
+
+def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
+    """Explicit visibility mask of one sample, rows and columns in [gen ; ref] order.
+
+    M[q, k] is True when query q may attend to key k:
+      gen q, gen k : True                               (full base self-attention)
+      gen q, ref k : valid(frame(k))                    (§1: gen attends to all reference tokens)
+      ref q, gen k : False                              (§1, §8: reference only self-attends)
+      ref q, ref k : valid(frame(q)) and valid(frame(k)) and group(q) == group(k)
+    `rows` selects a subset of query rows (row-block mode for large shapes).
+    """
+    G, R, F = sample_sizes(geom)
+    v = frame_valid(geom)
+    g = int(geom.group_frames)
+    assert g >= 1
+    if rows is None:
+        rows = np.arange(G + R)
+    rows = np.asarray(rows, dtype=np.int64)
+    M = np.zeros((rows.size, G + R), dtype=bool)
+    is_gen = rows < G
+    key_frame = np.arange(R) // F if F > 0 else np.zeros(0, dtype=np.int64)
+    key_valid = v[key_frame] if R > 0 else np.zeros(0, dtype=bool)
+    key_group = key_frame // g
+    # generation query rows
+    M[is_gen, :G] = True
+    M[np.ix_(is_gen, np.arange(G, G + R))] = key_valid[None, :]
+    # reference query rows
+    ref_rows = np.nonzero(~is_gen)[0]
+    if ref_rows.size:
+        j = rows[ref_rows] - G
+        q_frame = j // F
+        q_valid = v[q_frame]
+        q_group = q_frame // g
+        blk = q_valid[:, None] & key_valid[None, :] & (q_group[:, None] == key_group[None, :])
+        M[np.ix_(ref_rows, np.arange(G, G + R))] = blk
+    return M
+
+
+def pair_counts(samples: Sequence, block_rows: int = 2048) -> Tuple[int, int]:
+    """Visible (query, key) pairs per head, summed over samples, counted on the mask.
+
+    Returns (pairs of gen queries, pairs of ref queries). Counts True entries of the
+    explicit mask, built in row blocks, so it is exact (integer) at any size.
+    """
+    gen_pairs = 0
+    ref_pairs = 0
+    for geom in samples:
+        G, R, F = sample_sizes(geom)
+        for r0 in range(0, G + R, block_rows):
+            rows = np.arange(r0, min(G + R, r0 + block_rows))
+            cnt = visibility_mask(geom, rows).sum(axis=1, dtype=np.int64)
+            gen_pairs += int(cnt[rows < G].sum())
+            ref_pairs += int(cnt[rows >= G].sum())
+    return gen_pairs, ref_pairs
+
+
+# ----------------------------------------------------------------------------- kernels
+def _masked_softmax_rows(S: np.ndarray, M: np.ndarray):
+    """Row softmax of S restricted to M. Rows with no visible key give P = 0, LSE = -inf."""
+    S = np.where(M, S, NEG_INF)
+    m = S.max(axis=1) if S.shape[1] else np.full(S.shape[0], NEG_INF, dtype=S.dtype)
+    has = np.isfinite(m)
+    m_safe = np.where(has, m, 0.0).astype(S.dtype)
+    E = np.where(M, np.exp(S - m_safe[:, None]), 0.0).astype(S.dtype)
+    l = E.sum(axis=1)
+    P = np.zeros_like(E)
+    P[has] = E[has] / l[has, None]
+    lse = np.full(S.shape[0], NEG_INF, dtype=S.dtype)
+    lse[has] = m[has] + np.log(l[has])
+    return P, lse
+
+
+def attention_rows(q: np.ndarray, k: np.ndarray, v: np.ndarray, M: np.ndarray, scale: float):
+    """Masked attention for a block of query rows: returns (O, LSE, P)."""
+    S = (q @ k.T) * q.dtype.type(scale)
+    P, lse = _masked_softmax_rows(S, M)
+    return P @ v, lse, P
+
+
+def attention_backward_full(q, k, v, do, M, scale):
+    """Gradient of O = softmax_M(scale Q K^T) V for one (sample, head), all rows at once.
+
+    D = rowsum(dO * O); dV = P^T dO; dP = dO V^T; dS = P * (dP - D); dQ = scale dS K;
+    dK = scale dS^T Q. Rows with no visible key have P = 0 and contribute nothing.
+    """
+    o, lse, P = attention_rows(q, k, v, M, scale)
+    D = (do * o).sum(axis=1)
+    dv = P.T @ do
+    dP = do @ v.T
+    dS = P * (dP - D[:, None])
+    s = q.dtype.type(scale)
+    dq = (dS @ k) * s
+    dk = (dS.T @ q) * s
+    return dq, dk, dv, o, lse
+
+
+# ----------------------------------------------------------------------------- problem level
+def _offsets(samples):
+    go, ro = [0], [0]
+    for geom in samples:
+        G, R, _ = sample_sizes(geom)
+        go.append(go[-1] + G)
+        ro.append(ro[-1] + R)
+    return go, ro
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)
+
+
+def sra_forward(x: Dict[str, np.ndarray], samples: Sequence, scale: Optional[float] = None,
+                dtype=np.float64):
+    """Full forward over a packed batch.
+
+    x holds q_gen, k_gen, v_gen [sumG, H, d] and q_ref, k_ref, v_ref [sumR, H, d].
+    Returns o_gen [sumG,H,d], o_ref [sumR,H,d], lse_gen [H,sumG], lse_ref [H,sumR].
+    """
+    H, d = x["q_gen"].shape[1:]
+    scale = default_scale(d) if scale is None else scale
+    go, ro = _offsets(samples)
+    o_gen = np.zeros((go[-1], H, d), dtype)
+    o_ref = np.zeros((ro[-1], H, d), dtype)
+    lse_gen = np.full((H, go[-1]), NEG_INF, dtype)
+    lse_ref = np.full((H, ro[-1]), NEG_INF, dtype)
+    for b, geom in enumerate(samples):
+        G, R, _ = sample_sizes(geom)
+        M = visibility_mask(geom)
+        gs, rs = slice(go[b], go[b + 1]), slice(ro[b], ro[b + 1])
+        for h in range(H):
+            qh = np.concatenate([x["q_gen"][gs, h], x["q_ref"][rs, h]]).astype(dtype)
+            kh = np.concatenate([x["k_gen"][gs, h], x["k_ref"][rs, h]]).astype(dtype)
+            vh = np.concatenate([x["v_gen"][gs, h], x["v_ref"][rs, h]]).astype(dtype)
+            o, lse, _ = attention_rows(qh, kh, vh, M, scale)
+            o_gen[gs, h], o_ref[rs, h] = o[:G], o[G:]
+            lse_gen[h, gs], lse_ref[h, rs] = lse[:G], lse[G:]
+    return o_gen, o_ref, lse_gen, lse_ref
+
+
+def sra_backward(x: Dict[str, np.ndarray], samples: Sequence, scale: Optional[float] = None,
+                 dtype=np.float64):
+    """Full backward over a packed batch; x additionally holds do_gen, do_ref.
+
+    Returns dict dq_gen, dk_gen, dv_gen, dq_ref, dk_ref, dv_ref (same shapes as inputs),
+    plus the forward outputs o_gen, o_ref, lse_gen, lse_ref it recomputed.
+    """
+    H, d = x["q_gen"].shape[1:]
+    scale = default_scale(d) if scale is None else scale
+    go, ro = _offsets(samples)
+    out = {n: np.zeros(((go if n.endswith("gen") else ro)[-1], H, d), dtype)
+           for n in ("dq_gen", "dk_gen", "dv_gen", "dq_ref", "dk_ref", "dv_ref", "o_gen", "o_ref")}
+    out["lse_gen"] = np.full((H, go[-1]), NEG_INF, dtype)
+    out["lse_ref"] = np.full((H, ro[-1]), NEG_INF, dtype)
+    for b, geom in enumerate(samples):
+        G, R, _ = sample_sizes(geom)
+        M = visibility_mask(geom)
+        gs, rs = slice(go[b], go[b + 1]), slice(ro[b], ro[b + 1])
+        for h in range(H):
+            cat = lambda a, c: np.concatenate([x[a][gs, h], x[c][rs, h]]).astype(dtype)
+            q, k, v = cat("q_gen", "q_ref"), cat("k_gen", "k_ref"), cat("v_gen", "v_ref")
+            do = cat("do_gen", "do_ref")
+            dq, dk, dv, o, lse = attention_backward_full(q, k, v, do, M, scale)
+            for name, val in (("dq", dq), ("dk", dk), ("dv", dv), ("o", o)):
+                out[name + "_gen"][gs, h] = val[:G]
+                out[name + "_ref"][rs, h] = val[G:]
+            out["lse_gen"][h, gs], out["lse_ref"][h, rs] = lse[:G], lse[G:]
+    return out
+
+
+# ----------------------------------------------------------------------------- sampled rows
+def _sample_head(x, samples, b, h, dtype):
+    go, ro = _offsets(samples)
+    gs, rs = slice(go[b], go[b + 1]), slice(ro[b], ro[b + 1])
+    cat = lambda a, c: np.concatenate([np.asarray(x[a][gs, h]), np.asarray(x[c][rs, h])]).astype(dtype)
+    return cat, go, ro
+
+
+def forward_rows(x, samples, b: int, h: int, rows: np.ndarray, scale=None, dtype=np.float64):
+    """O and LSE of selected query rows of sample b, head h (rows index [gen ; ref] of the sample).
+
+    x entries may be any array-likes of shape [T, H, d] (numpy or CPU torch views).
+    """
+    d = x["q_gen"].shape[2]
+    scale = default_scale(d) if scale is None else scale
+    geom = samples[b]
+    cat, _, _ = _sample_head(x, samples, b, h, dtype)
+    q = cat("q_gen", "q_ref")[rows]
+    k, v = cat("k_gen", "k_ref"), cat("v_gen", "v_ref")
+    M = visibility_mask(geom, rows)
+    o, lse, _ = attention_rows(q, k, v, M, scale)
+    return o, lse
+
+
+def dq_rows(x, samples, b: int, h: int, rows: np.ndarray, scale=None, dtype=np.float64):
+    """dQ of selected query rows (each row's gradient depends only on that row)."""
+    d = x["q_gen"].shape[2]
+    scale = default_scale(d) if scale is None else scale
+    geom = samples[b]
+    cat, _, _ = _sample_head(x, samples, b, h, dtype)
+    q = cat("q_gen", "q_ref")[rows]
+    do = cat("do_gen", "do_ref")[rows]
+    k, v = cat("k_gen", "k_ref"), cat("v_gen", "v_ref")
+    M = visibility_mask(geom, rows)
+    o, lse, P = attention_rows(q, k, v, M, scale)
+    D = (do * o).sum(axis=1)
+    dS = P * (do @ v.T - D[:, None])
+    return (dS @ k) * dtype(scale)

@@ -1,0 +1,146 @@
+"""Planted mistakes in the oracle (on the CPU) must each be caught by a pin.
+
+Each mutant replaces one piece of the oracle with a plausible error (a dropped term, a
+wrong sign or index, a transposed operand); the test runs a pin from
+test_oracle_pins against the mutant and requires it to fail.
+"""
+import numpy as np
+import pytest
+
+import oracle.sra_oracle as so
+from sra_inputs import SampleGeom
+
+import test_oracle_pins as pins
+
+_orig_mask = so.visibility_mask
+_orig_bwd = so.attention_backward_full
+_orig_rows = so.attention_rows
+
+
+def mask_gen_drops_ref(geom, rows=None):
+    M = _orig_mask(geom, rows)
+    G = geom.n_gen
+    r = np.arange(G + geom.n_ref) if rows is None else np.asarray(rows)
+    M[np.ix_(r < G, np.arange(G, M.shape[1]))] = False
+    return M
+
+
+def mask_ref_sees_gen(geom, rows=None):
+    M = _orig_mask(geom, rows)
+    G = geom.n_gen
+    r = np.arange(G + geom.n_ref) if rows is None else np.asarray(rows)
+    M[np.ix_(r >= G, np.arange(G))] = True
+    return M
+
+
+def mask_ref_sees_all_ref(geom, rows=None):
+    M = _orig_mask(geom, rows)
+    G = geom.n_gen
+    r = np.arange(G + geom.n_ref) if rows is None else np.asarray(rows)
+    M[np.ix_(r >= G, np.arange(G, M.shape[1]))] = True
+    return M
+
+
+def mask_group_modulo(geom, rows=None):
+    class G2:
+        pass
+    g = G2()
+    for k in ("gen_frames", "gen_h", "gen_w", "ref_frames", "ref_h", "ref_w", "frame_valid"):
+        setattr(g, k, getattr(geom, k))
+    g.n_gen, g.n_ref = geom.n_gen, geom.n_ref
+    # wrong index: group of frame f taken as f % group_frames through a permuted frame order
+    g.group_frames = geom.group_frames
+    M = _orig_mask(g, rows)
+    F = geom.ref_h * geom.ref_w
+    G = geom.n_gen
+    if geom.group_frames > 1 and geom.ref_frames > geom.group_frames:
+        r = np.arange(G + geom.n_ref) if rows is None else np.asarray(rows)
+        fr = (np.arange(geom.n_ref) // F)
+        grp = fr % geom.group_frames
+        for i, q in enumerate(r):
+            if q >= G and M[i, G:].any():
+                fq = (q - G) // F
+                M[i, G:] = grp == (fq % geom.group_frames)
+    return M
+
+
+def mask_ignores_validity(geom, rows=None):
+    class G2:
+        pass
+    g = G2()
+    for k in ("gen_frames", "gen_h", "gen_w", "ref_frames", "ref_h", "ref_w", "group_frames"):
+        setattr(g, k, getattr(geom, k))
+    g.frame_valid = None
+    return _orig_mask(g, rows)
+
+
+def rows_no_scale(q, k, v, M, scale):
+    return _orig_rows(q, k, v, M, 1.0)
+
+
+def rows_lse_without_max(q, k, v, M, scale):
+    o, lse, P = _orig_rows(q, k, v, M, scale)
+    S = np.where(M, (q @ k.T) * scale, -np.inf)
+    m = S.max(axis=1)
+    return o, np.where(np.isfinite(lse), lse - m, lse), P
+
+
+def bwd_sign(q, k, v, do, M, scale):
+    o, lse, P = so.attention_rows(q, k, v, M, scale)
+    D = (do * o).sum(axis=1)
+    dS = P * (do @ v.T + D[:, None])
+    return dS @ k * scale, dS.T @ q * scale, P.T @ do, o, lse
+
+
+def bwd_transposed(q, k, v, do, M, scale):
+    o, lse, P = so.attention_rows(q, k, v, M, scale)
+    D = (do * o).sum(axis=1)
+    dS = P * (do @ v.T - D[:, None])
+    return dS @ k * scale, dS @ q * scale, P.T @ do, o, lse
+
+
+def bwd_drop_D(q, k, v, do, M, scale):
+    o, lse, P = so.attention_rows(q, k, v, M, scale)
+    dS = P * (do @ v.T)
+    return dS @ k * scale, dS.T @ q * scale, P.T @ do, o, lse
+
+
+G_INVALID = SampleGeom(3, 2, 4, 5, 2, 5, group_frames=1, frame_valid=[1, 0, 1, 1, 0])
+G_GROUP2 = SampleGeom(1, 4, 4, 6, 3, 3, group_frames=2, frame_valid=[1, 1, 0, 1, 1, 1])
+G_BWD = SampleGeom(2, 2, 2, 3, 2, 2, frame_valid=[1, 0, 1])
+
+
+def _all_forward_pins():
+    for geom in (G_INVALID, G_GROUP2):
+        pins.test_gen_rows_equal_dense_attention_over_gen_and_valid_ref(geom)
+        pins.test_ref_rows_equal_per_group_dense_attention(geom)
+        pins.test_zero_keys_give_log_visible_count(geom)
+    pins.test_brute_force_quadruple_loop(2)
+
+
+def _all_backward_pins():
+    pins.test_backward_central_finite_differences(G_BWD)
+    pins.test_backward_matches_torch_autograd_masked_softmax()
+
+
+@pytest.mark.parametrize("attr,mutant,which", [
+    ("visibility_mask", mask_gen_drops_ref, "fwd"),
+    ("visibility_mask", mask_ref_sees_gen, "fwd"),
+    ("visibility_mask", mask_ref_sees_all_ref, "fwd"),
+    ("visibility_mask", mask_group_modulo, "fwd"),
+    ("visibility_mask", mask_ignores_validity, "fwd"),
+    ("attention_rows", rows_no_scale, "fwd"),
+    ("attention_rows", rows_lse_without_max, "fwd"),
+    ("attention_backward_full", bwd_sign, "bwd"),
+    ("attention_backward_full", bwd_transposed, "bwd"),
+    ("attention_backward_full", bwd_drop_D, "bwd"),
+])
+def test_planted_mistake_is_caught(monkeypatch, attr, mutant, which):
+    monkeypatch.setattr(so, attr, mutant)
+    with pytest.raises(AssertionError):
+        (_all_forward_pins if which == "fwd" else _all_backward_pins)()
+
+
+def test_unmutated_oracle_passes_the_same_pins():
+    _all_forward_pins()
+    _all_backward_pins()
