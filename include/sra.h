@@ -1,0 +1,152 @@
+/*
+ * sra.h — C ABI of libsra: Sparse Reference Attention (SRA) on AMD Instinct MI355X (gfx950).
+ *
+ * SRA is the asymmetric attention of Avatar V (§1 contributions; §2.1 "Sparse Reference
+ * Attention"; §4.3 reference KV caching and invalid-token skipping; §8 related work):
+ *   - every generation (gen) query attends to all gen keys of its sample and to every valid
+ *     reference (ref) key of its sample, through ONE softmax over the concatenated key set
+ *     (§4.3 concatenates the cached reference K/V with the generation K/V);
+ *   - every ref query attends only to the ref keys of its own self-attention group, never to
+ *     gen keys (§1, §8: reference tokens only self-attend). A group is `group_frames`
+ *     consecutive reference latent frames; group_frames = 1 keeps the cost linear in the
+ *     reference length (§1, §2.1);
+ *   - tokens of invalid reference frames (§4.3, e.g. frames where the face is not visible)
+ *     are neither keys nor queries: their outputs are 0, their log-sum-exp is -inf and
+ *     their gradients are 0.
+ * Samples of a packed (varlen) batch never see each other.
+ *
+ * Conventions shared by every entry point
+ *   Tensors   bf16 tensors are [tokens, heads, head_dim] with head stride head_dim and element
+ *             stride 1. Tokens of all samples are packed back to back in sample order, and
+ *             frame-major (frame, row, column) inside a sample. q/k/v of a stream use that
+ *             stream's token stride (elements between consecutive tokens, >= heads*head_dim,
+ *             so q/k/v packed into one buffer work); o, do, dq, dk, dv are dense
+ *             (token stride heads*head_dim). lse tensors are fp32 [heads, tokens], natural log.
+ *   Memory    every data pointer and the workspace are DEVICE pointers owned by the caller.
+ *             The library allocates no device memory. It owns pinned host staging buffers for
+ *             its cached schedules (freed by sra_release_caches or at process exit).
+ *   Streams   `stream` is a hipStream_t (NULL = the default stream). Calls only enqueue work
+ *             on it and never synchronise the device.
+ *   Errors    every argument is validated before anything is enqueued, so a call that
+ *             returns an error has written nothing. sra_last_error() gives a per-thread
+ *             message. No C++ exception crosses this boundary. All functions are thread safe.
+ *   Supported head_dim in {64, 128}; heads >= 1; batch >= 1; every sample has >= 1 gen token.
+ */
+#ifndef SRA_H_
+#define SRA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum sra_status {
+  SRA_OK = 0,
+  SRA_ERR_INVALID_ARGUMENT = 1,     /* bad geometry, null pointer, stride, flag, ...           */
+  SRA_ERR_UNSUPPORTED = 2,          /* valid request the library does not implement (head_dim) */
+  SRA_ERR_WORKSPACE_TOO_SMALL = 3,  /* workspace_bytes below sra_workspace_size()              */
+  SRA_ERR_HIP = 4,                  /* the HIP runtime reported an error while enqueuing       */
+  SRA_ERR_INTERNAL = 5              /* host allocation failure or internal inconsistency       */
+} sra_status;
+
+/* Geometry of one sample (host memory). Gen tokens G = gen_frames*gen_h*gen_w (>= 1);
+ * ref tokens R = ref_frames*ref_h*ref_w (>= 0); F = ref_h*ref_w tokens per ref frame. */
+typedef struct sra_sample_geom {
+  int32_t gen_frames, gen_h, gen_w;
+  int32_t ref_frames, ref_h, ref_w;
+  int32_t group_frames;              /* >= 1: ref frames per ref self-attention group          */
+  const uint8_t* ref_frame_valid;    /* host, ref_frames bytes (0 = invalid); NULL = all valid */
+} sra_sample_geom;
+
+typedef struct sra_problem {
+  int32_t batch;                     /* samples in the packed batch, >= 1                      */
+  int32_t num_heads;                 /* H >= 1 (same for Q, K and V)                           */
+  int32_t head_dim;                  /* d in {64, 128}                                         */
+  float softmax_scale;               /* <= 0 selects 1/sqrt(head_dim)                          */
+  const sra_sample_geom* samples;    /* host array [batch]                                     */
+  int64_t gen_token_stride;          /* elements between gen q/k/v tokens; 0 selects H*d       */
+  int64_t ref_token_stride;          /* elements between ref q/k/v tokens; 0 selects H*d       */
+  uint32_t flags;                    /* must be 0 (reserved)                                   */
+} sra_problem;
+
+/* Which schedule an inspection hook looks at. */
+enum {
+  SRA_SCHED_FORWARD = 0,   /* query tiles -> key spans (forward pass)                 */
+  SRA_SCHED_BWD_DQ = 1,    /* query tiles -> key spans (dQ kernel of the backward)    */
+  SRA_SCHED_BWD_DKDV = 2   /* key tiles -> query spans (dK/dV kernel of the backward) */
+};
+
+/* Bytes of device workspace sra_forward (backward = 0) or sra_backward (backward = 1) needs
+ * for problem `p`. Writes *bytes; host only, enqueues nothing. */
+sra_status sra_workspace_size(const sra_problem* p, int backward, size_t* bytes);
+
+/* Forward pass of SRA (the definition at the top of this file).
+ * In : q_gen, k_gen, v_gen  bf16 [sumG, H, d] (gen token stride);
+ *      q_ref, k_ref, v_ref  bf16 [sumR, H, d] (ref token stride); may be NULL when sumR = 0.
+ * Out: o_gen bf16 [sumG, H, d], o_ref bf16 [sumR, H, d] (dense);
+ *      lse_gen fp32 [H, sumG], lse_ref fp32 [H, sumR]: natural-log log-sum-exp of the scaled
+ *      logits of each query row (-inf for rows of invalid frames).
+ * workspace: device buffer of at least sra_workspace_size(p, 0) bytes, 256-byte aligned; its
+ * contents are scratch and need no initialisation. Every output element is written. */
+sra_status sra_forward(const sra_problem* p,
+                       const void* q_gen, const void* k_gen, const void* v_gen,
+                       const void* q_ref, const void* k_ref, const void* v_ref,
+                       void* o_gen, void* o_ref, float* lse_gen, float* lse_ref,
+                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* Backward pass: gradients of the forward outputs o_gen/o_ref with respect to every input,
+ * given the upstream gradients do_gen/do_ref (bf16, dense, same shapes as o) and the forward's
+ * o and lse (as sra_forward wrote them). Writes dq/dk/dv for both streams (bf16, dense,
+ * same shapes as q/k/v); it overwrites them and does not accumulate. Gradients of tokens of
+ * invalid frames are 0. Internally: D = rowsum(dO * O) in fp32, then the dK/dV and dQ
+ * products of the softmax gradient with fp32 accumulation.
+ * workspace: at least sra_workspace_size(p, 1) bytes, 256-byte aligned, no initialisation. */
+sra_status sra_backward(const sra_problem* p,
+                        const void* q_gen, const void* k_gen, const void* v_gen,
+                        const void* q_ref, const void* k_ref, const void* v_ref,
+                        const void* o_gen, const void* o_ref,
+                        const float* lse_gen, const float* lse_ref,
+                        const void* do_gen, const void* do_ref,
+                        void* dq_gen, void* dk_gen, void* dv_gen,
+                        void* dq_ref, void* dk_ref, void* dv_ref,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* ---- host-only inspection hooks (no device needed; used to test the schedules) ---------- */
+
+/* Visible (query, key) pairs per head summed over samples, from the closed form
+ * G*(G + R_valid) for gen queries and sum over groups of (valid tokens of the group)^2 for
+ * ref queries. Either output pointer may be NULL. */
+sra_status sra_pair_counts(const sra_problem* p, int64_t* gen_pairs, int64_t* ref_pairs);
+
+/* Sizes of schedule `which` (SRA_SCHED_*): work items (all heads) and span entries, and the
+ * (query, key) pairs the schedule covers per head (must equal the pair count). */
+sra_status sra_schedule_info(const sra_problem* p, int which, int64_t* n_items,
+                             int64_t* n_spans, int64_t* covered_pairs);
+
+/* Expands schedule `which` for head 0 of `sample` into a (G+R) x (G+R) byte matrix, rows =
+ * queries and columns = keys in [gen ; ref] order of that sample: out[q*(G+R)+k] = number of
+ * work items that compute the pair (q, k), so a correct schedule gives exactly the 0/1
+ * visibility mask. out must hold (G+R)^2 bytes (host). */
+sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, uint8_t* out);
+
+/* Copies schedule `which` into host buffers: items[8*i + 0..7] = {stream, head, start, length,
+ * span_offset, span_count, sample, reserved} per work item, spans[4*j + 0..3] = {stream,
+ * start, length, reserved} per span (stream 0 = gen, 1 = ref; start = packed token row).
+ * items/spans may be NULL to query only; capacities count int32 elements. */
+sra_status sra_schedule_export(const sra_problem* p, int which, int32_t* items,
+                               int64_t items_capacity, int32_t* spans, int64_t spans_capacity);
+
+/* Frees cached schedules and their pinned host buffers, after waiting for the copies that
+ * read them. Safe to call at any time; later calls rebuild what they need. */
+sra_status sra_release_caches(void);
+
+const char* sra_status_string(sra_status s);
+const char* sra_last_error(void);   /* per-thread detail of the last failing call ("" if none) */
+int32_t sra_version(void);          /* major*10000 + minor*100 + patch                         */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SRA_H_ */

@@ -1,0 +1,275 @@
+// Geometry -> visibility runs -> tile schedules (host).
+//
+// Visibility (Avatar V §1, §2.1, §4.3, §8): a gen query sees every gen key of its sample and
+// every key of a valid ref frame of its sample; a ref query of a valid frame sees the keys
+// of the valid frames of its own group of `group_frames` frames. The rule is expressed
+// here as contiguous row ranges ("spans"), so each work item's kernel loop visits only
+// visible key (or query) rows and masks nothing but the ragged end of a span.
+#include "schedule.hpp"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <numeric>
+
+namespace sra {
+
+namespace {
+
+struct Run {  // [f0, f1) frames, all valid
+  int32_t f0, f1;
+};
+
+// Maximal runs of valid frames inside [lo, hi).
+std::vector<Run> valid_runs(const SampleLayout& s, int32_t lo, int32_t hi) {
+  std::vector<Run> runs;
+  int32_t f = lo;
+  while (f < hi) {
+    while (f < hi && !s.valid[f]) ++f;
+    if (f >= hi) break;
+    int32_t g = f;
+    while (g < hi && s.valid[g]) ++g;
+    runs.push_back({f, g});
+    f = g;
+  }
+  return runs;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t lim) { return a >= 0 && b >= 0 && (b == 0 || a <= lim / b); }
+
+}  // namespace
+
+sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
+  if (!p) { *err = "problem is NULL"; return SRA_ERR_INVALID_ARGUMENT; }
+  if (p->batch < 1) { *err = "batch must be >= 1"; return SRA_ERR_INVALID_ARGUMENT; }
+  if (p->num_heads < 1) { *err = "num_heads must be >= 1"; return SRA_ERR_INVALID_ARGUMENT; }
+  if (p->head_dim != 64 && p->head_dim != 128) {
+    *err = "head_dim " + std::to_string(p->head_dim) + " unsupported (64 or 128)";
+    return p->head_dim > 0 ? SRA_ERR_UNSUPPORTED : SRA_ERR_INVALID_ARGUMENT;
+  }
+  if (!p->samples) { *err = "samples is NULL"; return SRA_ERR_INVALID_ARGUMENT; }
+  if (p->flags != 0) { *err = "flags must be 0"; return SRA_ERR_INVALID_ARGUMENT; }
+  if (!(std::isfinite(p->softmax_scale))) { *err = "softmax_scale is not finite"; return SRA_ERR_INVALID_ARGUMENT; }
+  const int64_t hd = int64_t(p->num_heads) * p->head_dim;
+  Layout L;
+  L.batch = p->batch;
+  L.heads = p->num_heads;
+  L.head_dim = p->head_dim;
+  L.scale = p->softmax_scale > 0.f ? p->softmax_scale : float(1.0 / std::sqrt(double(p->head_dim)));
+  L.gen_stride = p->gen_token_stride == 0 ? hd : p->gen_token_stride;
+  L.ref_stride = p->ref_token_stride == 0 ? hd : p->ref_token_stride;
+  if (L.gen_stride < hd || L.ref_stride < hd) {
+    *err = "token stride must be >= num_heads*head_dim";
+    return SRA_ERR_INVALID_ARGUMENT;
+  }
+  const int64_t kRowLimit = (int64_t(1) << 31) - 1;
+  L.samples.resize(p->batch);
+  for (int32_t b = 0; b < p->batch; ++b) {
+    const sra_sample_geom& g = p->samples[b];
+    SampleLayout& s = L.samples[b];
+    const std::string tag = "sample " + std::to_string(b) + ": ";
+    if (g.gen_frames < 1 || g.gen_h < 1 || g.gen_w < 1) {
+      *err = tag + "generation frames/height/width must be >= 1";
+      return SRA_ERR_INVALID_ARGUMENT;
+    }
+    if (g.ref_frames < 0 || g.ref_h < 0 || g.ref_w < 0 || (g.ref_frames > 0 && (g.ref_h < 1 || g.ref_w < 1))) {
+      *err = tag + "reference frames must be >= 0 and height/width >= 1 when frames > 0";
+      return SRA_ERR_INVALID_ARGUMENT;
+    }
+    if (g.group_frames < 1) { *err = tag + "group_frames must be >= 1"; return SRA_ERR_INVALID_ARGUMENT; }
+    if (!mul_ok(g.gen_frames, int64_t(g.gen_h) * g.gen_w, kRowLimit) ||
+        !mul_ok(g.ref_frames, int64_t(g.ref_h) * g.ref_w, kRowLimit)) {
+      *err = tag + "token count overflows int32";
+      return SRA_ERR_INVALID_ARGUMENT;
+    }
+    s.G = int64_t(g.gen_frames) * g.gen_h * g.gen_w;
+    s.F = g.ref_frames > 0 ? int64_t(g.ref_h) * g.ref_w : 0;
+    s.R = int64_t(g.ref_frames) * s.F;
+    s.ref_frames = g.ref_frames;
+    s.group = g.group_frames;
+    s.valid.assign(g.ref_frames, 1);
+    if (g.ref_frame_valid)
+      for (int32_t f = 0; f < g.ref_frames; ++f) s.valid[f] = g.ref_frame_valid[f] ? 1 : 0;
+    s.gen_off = L.sum_gen;
+    s.ref_off = L.sum_ref;
+    L.sum_gen += s.G;
+    L.sum_ref += s.R;
+    if (L.sum_gen > kRowLimit || L.sum_ref > kRowLimit) {
+      *err = "packed token count overflows int32";
+      return SRA_ERR_INVALID_ARGUMENT;
+    }
+  }
+  *out = std::move(L);
+  return SRA_OK;
+}
+
+void closed_form_pairs(const Layout& L, int64_t* gen_pairs, int64_t* ref_pairs) {
+  int64_t gp = 0, rp = 0;
+  for (const SampleLayout& s : L.samples) {
+    int64_t valid_frames = std::accumulate(s.valid.begin(), s.valid.end(), int64_t(0));
+    gp += s.G * (s.G + valid_frames * s.F);
+    for (int32_t g0 = 0; g0 < s.ref_frames; g0 += s.group) {
+      int64_t n = 0;
+      for (int32_t f = g0; f < std::min(s.ref_frames, g0 + s.group); ++f) n += s.valid[f];
+      rp += (n * s.F) * (n * s.F);
+    }
+  }
+  if (gen_pairs) *gen_pairs = gp;
+  if (ref_pairs) *ref_pairs = rp;
+}
+
+namespace {
+
+struct TileClass {   // tiles sharing one span list
+  int32_t stream;
+  int64_t row0, rows;            // packed rows covered (tiled)
+  int32_t span_off, span_cnt;
+  int32_t sample;
+  int64_t other_rows;            // total rows over the span list
+};
+
+// Tiles rows [row0, row0+rows) of `stream` with `tile` rows each; one item per tile and head.
+void emit_items(const TileClass& c, int tile, int32_t heads, int step,
+                const std::vector<Span>& spans, std::vector<std::pair<int64_t, WorkItem>>* out) {
+  int64_t step_rows = 0;  // work estimate: span rows rounded up to the inner step
+  for (int32_t i = 0; i < c.span_cnt; ++i) {
+    int64_t l = spans[c.span_off + i].len;
+    step_rows += (l + step - 1) / step * step;
+  }
+  for (int32_t h = 0; h < heads; ++h)
+    for (int64_t r = 0; r < c.rows; r += tile) {
+      WorkItem w;
+      w.stream = c.stream;
+      w.head = h;
+      w.start = int32_t(c.row0 + r);
+      w.len = int32_t(std::min<int64_t>(tile, c.rows - r));
+      w.span_off = c.span_off;
+      w.span_cnt = c.span_cnt;
+      w.sample = c.sample;
+      w.reserved = 0;
+      out->push_back({int64_t(tile) * step_rows, w});
+    }
+}
+
+// Orders items for launch. Workgroups are dealt round-robin over the 8 XCDs, so item k of
+// the launch order runs on XCD k % 8 and each XCD consumes its own subsequence in order.
+// When heads divide evenly over the XCDs, every head is pinned to one XCD (its K/V stay in
+// that XCD's L2) and each XCD's subsequence is longest-first; otherwise the whole list is
+// longest-first and the round-robin deal balances it.
+void order_items(std::vector<std::pair<int64_t, WorkItem>>& v, int32_t heads, Schedule* s) {
+  std::stable_sort(v.begin(), v.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
+  s->real_items = int64_t(v.size());
+  s->items.clear();
+  if (heads % kNumXcd != 0 || v.empty()) {
+    for (auto& e : v) s->items.push_back(e.second);
+    return;
+  }
+  std::vector<std::vector<WorkItem>> per(kNumXcd);
+  for (auto& e : v) per[e.second.head % kNumXcd].push_back(e.second);
+  size_t n = 0;
+  for (auto& q : per) n = std::max(n, q.size());
+  WorkItem pad{};
+  pad.stream = -1;
+  for (size_t j = 0; j < n; ++j)
+    for (int x = 0; x < kNumXcd; ++x) s->items.push_back(j < per[x].size() ? per[x][j] : pad);
+}
+
+// Query-major schedule (forward and dQ): query tiles of `tile` rows, key spans per class.
+void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
+  std::vector<TileClass> classes;
+  s->spans.clear();
+  for (int32_t b = 0; b < L.batch; ++b) {
+    const SampleLayout& sm = L.samples[b];
+    // gen queries: gen keys + every valid ref run
+    TileClass c{0, sm.gen_off, sm.G, int32_t(s->spans.size()), 0, b, 0};
+    s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
+    for (const Run& r : valid_runs(sm, 0, sm.ref_frames))
+      s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
+    c.span_cnt = int32_t(s->spans.size()) - c.span_off;
+    classes.push_back(c);
+    // ref queries: per group, keys = valid runs of the group; query tiles per valid run
+    for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
+      std::vector<Run> runs = valid_runs(sm, g0, std::min(sm.ref_frames, g0 + sm.group));
+      if (runs.empty()) continue;
+      int32_t off = int32_t(s->spans.size());
+      for (const Run& r : runs)
+        s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
+      for (const Run& r : runs)
+        classes.push_back({1, sm.ref_off + r.f0 * sm.F, (r.f1 - r.f0) * sm.F, off, int32_t(runs.size()), b, 0});
+    }
+  }
+  std::vector<std::pair<int64_t, WorkItem>> v;
+  for (const TileClass& c : classes) emit_items(c, tile, L.heads, step, s->spans, &v);
+  order_items(v, L.heads, s);
+}
+
+// Key-major schedule (dK/dV): key tiles, query spans per class.
+void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
+  std::vector<TileClass> classes;
+  s->spans.clear();
+  for (int32_t b = 0; b < L.batch; ++b) {
+    const SampleLayout& sm = L.samples[b];
+    // gen keys are seen by the gen queries of the sample only
+    int32_t gq = int32_t(s->spans.size());
+    s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
+    classes.push_back({0, sm.gen_off, sm.G, gq, 1, b, 0});
+    // ref keys of a valid frame: gen queries + ref queries of the valid frames of its group
+    for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
+      std::vector<Run> runs = valid_runs(sm, g0, std::min(sm.ref_frames, g0 + sm.group));
+      if (runs.empty()) continue;
+      int32_t off = int32_t(s->spans.size());
+      s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
+      for (const Run& r : runs)
+        s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
+      for (const Run& r : runs)
+        classes.push_back({1, sm.ref_off + r.f0 * sm.F, (r.f1 - r.f0) * sm.F, off, int32_t(runs.size()) + 1, b, 0});
+    }
+  }
+  std::vector<std::pair<int64_t, WorkItem>> v;
+  for (const TileClass& c : classes) emit_items(c, tile, L.heads, step, s->spans, &v);
+  order_items(v, L.heads, s);
+}
+
+}  // namespace
+
+void build_plan(const Layout& L, Plan* plan) {
+  plan->layout = L;
+  build_query_major(L, kFwdQueryTile, kFwdKeyStep, &plan->fwd);
+  build_query_major(L, kDqQueryTile, kDqKeyStep, &plan->dq);
+  build_key_major(L, kDkvKeyTile, kDkvQueryStep, &plan->dkv);
+  plan->fill.clear();
+  for (const SampleLayout& sm : L.samples) {
+    int32_t f = 0;
+    while (f < sm.ref_frames) {
+      if (sm.valid[f]) { ++f; continue; }
+      int32_t g = f;
+      while (g < sm.ref_frames && !sm.valid[g]) ++g;
+      plan->fill.push_back({1, int32_t(sm.ref_off + f * sm.F), int32_t((g - f) * sm.F), 0});
+      f = g;
+    }
+  }
+}
+
+int64_t covered_pairs(const Schedule& s, bool /*key_major*/) {
+  int64_t n = 0;
+  for (const WorkItem& w : s.items) {
+    if (w.stream < 0 || w.head != 0) continue;
+    int64_t other = 0;
+    for (int32_t i = 0; i < w.span_cnt; ++i) other += s.spans[w.span_off + i].len;
+    n += int64_t(w.len) * other;
+  }
+  return n;
+}
+
+std::string layout_key(const Layout& L) {
+  std::string k;
+  auto put = [&k](int64_t v) { k.append(reinterpret_cast<const char*>(&v), sizeof v); };
+  put(L.batch); put(L.heads); put(L.head_dim);
+  for (const SampleLayout& s : L.samples) {
+    put(s.G); put(s.R); put(s.F); put(s.ref_frames); put(s.group);
+    k.append(reinterpret_cast<const char*>(s.valid.data()), s.valid.size());
+  }
+  return k;
+}
+
+}  // namespace sra

@@ -1,0 +1,58 @@
+// Host-side geometry validation and tile scheduling for Sparse Reference Attention.
+// Pure C++ (no HIP): turns per-sample frame geometry into work-item tables.
+#pragma once
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "sra.h"
+#include "sra_config.h"
+
+namespace sra {
+
+// Derived geometry of one sample.
+struct SampleLayout {
+  int64_t G = 0, R = 0, F = 0;        // gen tokens, ref tokens, tokens per ref frame
+  int64_t gen_off = 0, ref_off = 0;   // first packed row of the sample in each stream
+  int32_t ref_frames = 0, group = 1;
+  std::vector<uint8_t> valid;         // per ref frame, 0/1
+};
+
+struct Layout {
+  int32_t batch = 0, heads = 0, head_dim = 0;
+  float scale = 0.f;
+  int64_t gen_stride = 0, ref_stride = 0;  // q/k/v token strides (elements)
+  int64_t sum_gen = 0, sum_ref = 0;
+  std::vector<SampleLayout> samples;
+};
+
+// A schedule: work items (already in launch order, padded for the XCD mapping) and spans.
+struct Schedule {
+  std::vector<WorkItem> items;
+  std::vector<Span> spans;
+  int64_t real_items = 0;
+};
+
+struct Plan {
+  Layout layout;
+  Schedule fwd, dq, dkv;
+  std::vector<FillRange> fill;   // invalid reference rows
+};
+
+// Validates `p` and derives the layout. Returns SRA_OK or an error with `err` set.
+sra_status make_layout(const sra_problem* p, Layout* out, std::string* err);
+
+// Closed-form visible pairs per head (summed over samples).
+void closed_form_pairs(const Layout& L, int64_t* gen_pairs, int64_t* ref_pairs);
+
+// Builds the three schedules and the fill list.
+void build_plan(const Layout& L, Plan* plan);
+
+// Pairs per head covered by a schedule (head 0 items only, so per head).
+int64_t covered_pairs(const Schedule& s, bool key_major);
+
+// Geometry key for the plan cache.
+std::string layout_key(const Layout& L);
+
+}  // namespace sra

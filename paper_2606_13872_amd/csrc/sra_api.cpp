@@ -1,0 +1,456 @@
+// C ABI of libsra (include/sra.h): validation, plan cache, workspace layout and launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <list>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "sra.h"
+#include "schedule.hpp"
+#include "sra_kernels.h"
+
+namespace {
+
+using namespace sra;
+
+thread_local std::string g_last_error;
+
+sra_status fail(sra_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Byte image of a set of tables, laid out back to back (each 256-byte aligned). The pinned
+// copy is made on first use by a launch, so sizes can be queried without a device.
+struct Blob {
+  std::vector<size_t> offsets;
+  std::vector<char> image;
+  size_t bytes = 0;
+  void* pinned = nullptr;  // hipHostMalloc'd copy of the image
+};
+
+struct CachedPlan {
+  Plan plan;
+  Blob fwd;   // fwd items | fwd spans | fill
+  Blob bwd;   // dq items | dq spans | dkv items | dkv spans | fill
+  // Runs when the cache has dropped the plan and no call holds it any more. An upload
+  // enqueued by an earlier call may still read the pinned images: wait for the device.
+  ~CachedPlan() {
+    if (fwd.pinned || bwd.pinned) (void)hipDeviceSynchronize();
+    if (fwd.pinned) (void)hipHostFree(fwd.pinned);
+    if (bwd.pinned) (void)hipHostFree(bwd.pinned);
+  }
+};
+
+template <class T>
+void put_table(Blob& b, const std::vector<T>& v) {
+  size_t off = align_up(b.image.size());
+  b.image.resize(off + v.size() * sizeof(T));
+  if (!v.empty()) std::memcpy(b.image.data() + off, v.data(), v.size() * sizeof(T));
+  b.offsets.push_back(off);
+  b.bytes = align_up(b.image.size());
+}
+
+class PlanCache {
+ public:
+
+  sra_status get(const Layout& L, std::shared_ptr<CachedPlan>* out) {
+    std::lock_guard<std::mutex> lk(mu_);
+    std::string key = layout_key(L);
+    auto it = map_.find(key);
+    if (it != map_.end()) {
+      lru_.splice(lru_.begin(), lru_, it->second.second);
+      *out = it->second.first;
+      return SRA_OK;
+    }
+    auto cp = std::make_shared<CachedPlan>();
+    build_plan(L, &cp->plan);
+    put_table(cp->fwd, cp->plan.fwd.items);
+    put_table(cp->fwd, cp->plan.fwd.spans);
+    put_table(cp->fwd, cp->plan.fill);
+    put_table(cp->bwd, cp->plan.dq.items);
+    put_table(cp->bwd, cp->plan.dq.spans);
+    put_table(cp->bwd, cp->plan.dkv.items);
+    put_table(cp->bwd, cp->plan.dkv.spans);
+    put_table(cp->bwd, cp->plan.fill);
+    if (map_.size() >= kMaxPlans) evict_one();
+    lru_.push_front(key);
+    map_[key] = {cp, lru_.begin()};
+    *out = cp;
+    return SRA_OK;
+  }
+
+  // Pinned staging copy of a blob, made once per plan (the image never changes afterwards).
+  sra_status pinned(Blob& b, void** out) {
+    std::lock_guard<std::mutex> lk(mu_);
+    if (!b.pinned && b.bytes) {
+      void* p = nullptr;
+      if (hipHostMalloc(&p, b.bytes, hipHostMallocDefault) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SRA_ERR_HIP, "hipHostMalloc of schedule staging failed");
+      }
+      std::memcpy(p, b.image.data(), b.image.size());
+      b.pinned = p;
+    }
+    *out = b.pinned;
+    return SRA_OK;
+  }
+
+  void clear() {
+    std::lock_guard<std::mutex> lk(mu_);
+    map_.clear();
+    lru_.clear();
+  }
+
+ private:
+  static constexpr size_t kMaxPlans = 256;
+  void evict_one() {
+    map_.erase(lru_.back());
+    lru_.pop_back();
+  }
+  std::mutex mu_;
+  std::list<std::string> lru_;
+  std::unordered_map<std::string, std::pair<std::shared_ptr<CachedPlan>, std::list<std::string>::iterator>> map_;
+};
+
+PlanCache& cache() {
+  static PlanCache* c = new PlanCache();  // never destroyed: HIP may be torn down first at exit
+  return *c;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+size_t fwd_workspace(const CachedPlan& cp) { return cp.fwd.bytes; }
+size_t bwd_workspace(const CachedPlan& cp, const Layout& L) {
+  size_t b = cp.bwd.bytes;
+  b += align_up(size_t(L.heads) * L.sum_gen * sizeof(float));
+  b += align_up(size_t(L.heads) * L.sum_ref * sizeof(float));
+  return b;
+}
+
+sra_status common_checks(const sra_problem* p, Layout* L, std::shared_ptr<CachedPlan>* cp) {
+  std::string err;
+  sra_status st = make_layout(p, L, &err);
+  if (st != SRA_OK) return fail(st, err);
+  if (L->gen_stride % 8 || L->ref_stride % 8)
+    return fail(SRA_ERR_INVALID_ARGUMENT, "token strides must be multiples of 8 elements");
+  st = cache().get(*L, cp);
+  return st;
+}
+
+sra_status check_tensors(const Layout& L, std::initializer_list<const void*> gen,
+                         std::initializer_list<const void*> ref) {
+  for (const void* t : gen) {
+    if (!t) return fail(SRA_ERR_INVALID_ARGUMENT, "a generation tensor pointer is NULL");
+    if (!aligned16(t)) return fail(SRA_ERR_INVALID_ARGUMENT, "tensor pointers must be 16-byte aligned");
+  }
+  if (L.sum_ref > 0)
+    for (const void* t : ref) {
+      if (!t) return fail(SRA_ERR_INVALID_ARGUMENT, "a reference tensor pointer is NULL");
+      if (!aligned16(t)) return fail(SRA_ERR_INVALID_ARGUMENT, "tensor pointers must be 16-byte aligned");
+    }
+  return SRA_OK;
+}
+
+sra_status hip_fail(hipError_t e, const char* what) {
+  return fail(SRA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+sra_status sra_workspace_size(const sra_problem* p, int backward, size_t* bytes) {
+  g_last_error.clear();
+  if (!bytes) return fail(SRA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  Layout L;
+  std::shared_ptr<CachedPlan> cp;
+  sra_status st = common_checks(p, &L, &cp);
+  if (st != SRA_OK) return st;
+  *bytes = backward ? bwd_workspace(*cp, L) : fwd_workspace(*cp);
+  return SRA_OK;
+}
+
+sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
+                       const void* q_ref, const void* k_ref, const void* v_ref, void* o_gen, void* o_ref,
+                       float* lse_gen, float* lse_ref, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  g_last_error.clear();
+  Layout L;
+  std::shared_ptr<CachedPlan> cp;
+  sra_status st = common_checks(p, &L, &cp);
+  if (st != SRA_OK) return st;
+  st = check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen}, {q_ref, k_ref, v_ref, o_ref, lse_ref});
+  if (st != SRA_OK) return st;
+  const size_t need = fwd_workspace(*cp);
+  if (workspace_bytes < need)
+    return fail(SRA_ERR_WORKSPACE_TOO_SMALL, "forward needs " + std::to_string(need) + " workspace bytes");
+  if (need && (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign)))
+    return fail(SRA_ERR_INVALID_ARGUMENT, "workspace must be non-NULL and 256-byte aligned");
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  {
+    void* src = nullptr;
+    st = cache().pinned(cp->fwd, &src);
+    if (st != SRA_OK) return st;
+    hipError_t e = hipMemcpyAsync(ws, src, cp->fwd.bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "schedule upload");
+  }
+  const Plan& P = cp->plan;
+  FwdArgs a{};
+  a.items = reinterpret_cast<const WorkItem*>(ws + cp->fwd.offsets[0]);
+  a.spans = reinterpret_cast<const Span*>(ws + cp->fwd.offsets[1]);
+  a.q[0] = static_cast<const __bf16*>(q_gen);
+  a.k[0] = static_cast<const __bf16*>(k_gen);
+  a.v[0] = static_cast<const __bf16*>(v_gen);
+  a.q[1] = static_cast<const __bf16*>(q_ref);
+  a.k[1] = static_cast<const __bf16*>(k_ref);
+  a.v[1] = static_cast<const __bf16*>(v_ref);
+  a.in_stride[0] = L.gen_stride;
+  a.in_stride[1] = L.ref_stride;
+  a.o[0] = static_cast<__bf16*>(o_gen);
+  a.o[1] = static_cast<__bf16*>(o_ref);
+  a.lse[0] = lse_gen;
+  a.lse[1] = lse_ref;
+  a.rows[0] = int32_t(L.sum_gen);
+  a.rows[1] = int32_t(L.sum_ref);
+  a.heads = L.heads;
+  a.scale_log2 = float(double(L.scale) * 1.4426950408889634);
+  hipError_t e = launch_forward(a, int(P.fwd.items.size()), L.head_dim, s);
+  if (e != hipSuccess) return hip_fail(e, "forward launch");
+  if (!P.fill.empty()) {
+    FillArgs f{};
+    f.ranges = reinterpret_cast<const FillRange*>(ws + cp->fwd.offsets[2]);
+    f.n_ranges = int32_t(P.fill.size());
+    f.heads = L.heads;
+    f.head_dim = L.head_dim;
+    f.t[0] = static_cast<__bf16*>(o_ref);
+    f.lse = lse_ref;
+    f.lse_rows = int32_t(L.sum_ref);
+    e = launch_fill(f, s);
+    if (e != hipSuccess) return hip_fail(e, "fill launch");
+  }
+  return SRA_OK;
+}
+
+sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
+                        const void* q_ref, const void* k_ref, const void* v_ref, const void* o_gen,
+                        const void* o_ref, const float* lse_gen, const float* lse_ref, const void* do_gen,
+                        const void* do_ref, void* dq_gen, void* dk_gen, void* dv_gen, void* dq_ref,
+                        void* dk_ref, void* dv_ref, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  Layout L;
+  std::shared_ptr<CachedPlan> cp;
+  sra_status st = common_checks(p, &L, &cp);
+  if (st != SRA_OK) return st;
+  st = check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen, do_gen, dq_gen, dk_gen, dv_gen},
+                     {q_ref, k_ref, v_ref, o_ref, lse_ref, do_ref, dq_ref, dk_ref, dv_ref});
+  if (st != SRA_OK) return st;
+  const size_t need = bwd_workspace(*cp, L);
+  if (workspace_bytes < need)
+    return fail(SRA_ERR_WORKSPACE_TOO_SMALL, "backward needs " + std::to_string(need) + " workspace bytes");
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign))
+    return fail(SRA_ERR_INVALID_ARGUMENT, "workspace must be non-NULL and 256-byte aligned");
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  void* src = nullptr;
+  st = cache().pinned(cp->bwd, &src);
+  if (st != SRA_OK) return st;
+  hipError_t e = hipMemcpyAsync(ws, src, cp->bwd.bytes, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "schedule upload");
+  float* delta_gen = reinterpret_cast<float*>(ws + cp->bwd.bytes);
+  float* delta_ref = reinterpret_cast<float*>(ws + cp->bwd.bytes + align_up(size_t(L.heads) * L.sum_gen * sizeof(float)));
+
+  DeltaArgs d{};
+  d.o[0] = static_cast<const __bf16*>(o_gen);
+  d.o[1] = static_cast<const __bf16*>(o_ref);
+  d.dout[0] = static_cast<const __bf16*>(do_gen);
+  d.dout[1] = static_cast<const __bf16*>(do_ref);
+  d.delta[0] = delta_gen;
+  d.delta[1] = delta_ref;
+  d.rows[0] = int32_t(L.sum_gen);
+  d.rows[1] = int32_t(L.sum_ref);
+  d.heads = L.heads;
+  e = launch_delta(d, L.head_dim, s);
+  if (e != hipSuccess) return hip_fail(e, "delta launch");
+
+  const Plan& P = cp->plan;
+  BwdArgs a{};
+  a.q[0] = static_cast<const __bf16*>(q_gen);
+  a.k[0] = static_cast<const __bf16*>(k_gen);
+  a.v[0] = static_cast<const __bf16*>(v_gen);
+  a.q[1] = static_cast<const __bf16*>(q_ref);
+  a.k[1] = static_cast<const __bf16*>(k_ref);
+  a.v[1] = static_cast<const __bf16*>(v_ref);
+  a.in_stride[0] = L.gen_stride;
+  a.in_stride[1] = L.ref_stride;
+  a.dout[0] = static_cast<const __bf16*>(do_gen);
+  a.dout[1] = static_cast<const __bf16*>(do_ref);
+  a.lse[0] = lse_gen;
+  a.lse[1] = lse_ref;
+  a.delta[0] = delta_gen;
+  a.delta[1] = delta_ref;
+  a.dq[0] = static_cast<__bf16*>(dq_gen);
+  a.dk[0] = static_cast<__bf16*>(dk_gen);
+  a.dv[0] = static_cast<__bf16*>(dv_gen);
+  a.dq[1] = static_cast<__bf16*>(dq_ref);
+  a.dk[1] = static_cast<__bf16*>(dk_ref);
+  a.dv[1] = static_cast<__bf16*>(dv_ref);
+  a.rows[0] = int32_t(L.sum_gen);
+  a.rows[1] = int32_t(L.sum_ref);
+  a.heads = L.heads;
+  a.scale = L.scale;
+  a.scale_log2 = float(double(L.scale) * 1.4426950408889634);
+
+  a.items = reinterpret_cast<const WorkItem*>(ws + cp->bwd.offsets[2]);
+  a.spans = reinterpret_cast<const Span*>(ws + cp->bwd.offsets[3]);
+  e = launch_dkv(a, int(P.dkv.items.size()), L.head_dim, s);
+  if (e != hipSuccess) return hip_fail(e, "dkv launch");
+  a.items = reinterpret_cast<const WorkItem*>(ws + cp->bwd.offsets[0]);
+  a.spans = reinterpret_cast<const Span*>(ws + cp->bwd.offsets[1]);
+  e = launch_dq(a, int(P.dq.items.size()), L.head_dim, s);
+  if (e != hipSuccess) return hip_fail(e, "dq launch");
+  if (!P.fill.empty()) {
+    FillArgs f{};
+    f.ranges = reinterpret_cast<const FillRange*>(ws + cp->bwd.offsets[4]);
+    f.n_ranges = int32_t(P.fill.size());
+    f.heads = L.heads;
+    f.head_dim = L.head_dim;
+    f.t[0] = static_cast<__bf16*>(dq_ref);
+    f.t[1] = static_cast<__bf16*>(dk_ref);
+    f.t[2] = static_cast<__bf16*>(dv_ref);
+    e = launch_fill(f, s);
+    if (e != hipSuccess) return hip_fail(e, "fill launch");
+  }
+  return SRA_OK;
+}
+
+sra_status sra_pair_counts(const sra_problem* p, int64_t* gen_pairs, int64_t* ref_pairs) {
+  g_last_error.clear();
+  Layout L;
+  std::string err;
+  sra_status st = make_layout(p, &L, &err);
+  if (st != SRA_OK) return fail(st, err);
+  closed_form_pairs(L, gen_pairs, ref_pairs);
+  return SRA_OK;
+}
+
+static const Schedule* pick(const Plan& P, int which) {
+  switch (which) {
+    case SRA_SCHED_FORWARD: return &P.fwd;
+    case SRA_SCHED_BWD_DQ: return &P.dq;
+    case SRA_SCHED_BWD_DKDV: return &P.dkv;
+    default: return nullptr;
+  }
+}
+
+sra_status sra_schedule_info(const sra_problem* p, int which, int64_t* n_items, int64_t* n_spans,
+                             int64_t* covered) {
+  g_last_error.clear();
+  Layout L;
+  std::string err;
+  sra_status st = make_layout(p, &L, &err);
+  if (st != SRA_OK) return fail(st, err);
+  Plan P;
+  build_plan(L, &P);
+  const Schedule* S = pick(P, which);
+  if (!S) return fail(SRA_ERR_INVALID_ARGUMENT, "unknown schedule");
+  if (n_items) *n_items = int64_t(S->items.size());
+  if (n_spans) *n_spans = int64_t(S->spans.size());
+  if (covered) *covered = covered_pairs(*S, which == SRA_SCHED_BWD_DKDV);
+  return SRA_OK;
+}
+
+sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, uint8_t* out) {
+  g_last_error.clear();
+  Layout L;
+  std::string err;
+  sra_status st = make_layout(p, &L, &err);
+  if (st != SRA_OK) return fail(st, err);
+  if (sample < 0 || sample >= L.batch) return fail(SRA_ERR_INVALID_ARGUMENT, "sample out of range");
+  if (!out) return fail(SRA_ERR_INVALID_ARGUMENT, "out is NULL");
+  Plan P;
+  build_plan(L, &P);
+  const Schedule* S = pick(P, which);
+  if (!S) return fail(SRA_ERR_INVALID_ARGUMENT, "unknown schedule");
+  const SampleLayout& sm = L.samples[sample];
+  const int64_t n = sm.G + sm.R;
+  std::memset(out, 0, size_t(n * n));
+  auto local = [&](int32_t stream, int64_t row) -> int64_t {  // packed row -> [gen ; ref] index
+    return stream == 0 ? row - sm.gen_off : sm.G + (row - sm.ref_off);
+  };
+  const bool key_major = which == SRA_SCHED_BWD_DKDV;
+  for (const WorkItem& w : S->items) {
+    if (w.stream < 0 || w.head != 0 || w.sample != sample) continue;
+    for (int32_t si = 0; si < w.span_cnt; ++si) {
+      const Span& sp = S->spans[w.span_off + si];
+      for (int32_t a = 0; a < w.len; ++a) {
+        const int64_t ta = local(w.stream, int64_t(w.start) + a);
+        for (int32_t b = 0; b < sp.len; ++b) {
+          const int64_t tb = local(sp.stream, int64_t(sp.start) + b);
+          if (ta < 0 || ta >= n || tb < 0 || tb >= n) return fail(SRA_ERR_INTERNAL, "schedule leaves its sample");
+          const int64_t q = key_major ? tb : ta, k = key_major ? ta : tb;
+          uint8_t& c = out[q * n + k];
+          if (c < 255) ++c;
+        }
+      }
+    }
+  }
+  return SRA_OK;
+}
+
+sra_status sra_schedule_export(const sra_problem* p, int which, int32_t* items, int64_t items_capacity,
+                               int32_t* spans, int64_t spans_capacity) {
+  g_last_error.clear();
+  Layout L;
+  std::string err;
+  sra_status st = make_layout(p, &L, &err);
+  if (st != SRA_OK) return fail(st, err);
+  Plan P;
+  build_plan(L, &P);
+  const Schedule* S = pick(P, which);
+  if (!S) return fail(SRA_ERR_INVALID_ARGUMENT, "unknown schedule");
+  if (items) {
+    if (items_capacity < int64_t(S->items.size()) * 8) return fail(SRA_ERR_INVALID_ARGUMENT, "items buffer too small");
+    std::memcpy(items, S->items.data(), S->items.size() * sizeof(WorkItem));
+  }
+  if (spans) {
+    if (spans_capacity < int64_t(S->spans.size()) * 4) return fail(SRA_ERR_INVALID_ARGUMENT, "spans buffer too small");
+    std::memcpy(spans, S->spans.data(), S->spans.size() * sizeof(Span));
+  }
+  return SRA_OK;
+}
+
+sra_status sra_release_caches(void) {
+  g_last_error.clear();
+  cache().clear();
+  return SRA_OK;
+}
+
+const char* sra_status_string(sra_status s) {
+  switch (s) {
+    case SRA_OK: return "SRA_OK";
+    case SRA_ERR_INVALID_ARGUMENT: return "SRA_ERR_INVALID_ARGUMENT";
+    case SRA_ERR_UNSUPPORTED: return "SRA_ERR_UNSUPPORTED";
+    case SRA_ERR_WORKSPACE_TOO_SMALL: return "SRA_ERR_WORKSPACE_TOO_SMALL";
+    case SRA_ERR_HIP: return "SRA_ERR_HIP";
+    case SRA_ERR_INTERNAL: return "SRA_ERR_INTERNAL";
+  }
+  return "SRA_ERR_UNKNOWN";
+}
+
+const char* sra_last_error(void) { return g_last_error.c_str(); }
+
+int32_t sra_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,70 @@
+// Device helpers for the gfx950 (CDNA4) SRA kernels: MFMA, LDS transpose reads, wave64
+// lane-pair reductions and the LDS swizzles.
+//
+// Lane layouts of V_MFMA_F32_32X32X16_BF16 used throughout (lane l of a wave64):
+//   A (32 x 16): lane l holds A[l%32][8*(l/32) + j], j = 0..7
+//   B (16 x 32): lane l holds B[8*(l/32) + j][l%32]
+//   C (32 x 32): register i of lane l holds C[8*(i/4) + 4*(l/32) + i%4][l%32]
+// So lanes l and l+32 share one output column and split its 32 rows between them.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sra {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+typedef bf16x4 __attribute__((address_space(3))) lds_bf16x4;
+
+__device__ __forceinline__ floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Combine a value held by lanes l and l^32 (the two halves of one MFMA output column).
+__device__ __forceinline__ float pair_max(float x) {
+  auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
+// DS_READ_B64_TR_B16: within each 16-lane group, lane j addresses row j/4, columns
+// 4*(j%4)..+3 of a 4 x 16 block of 16-bit values; lane i receives column i (4 rows).
+__device__ __forceinline__ bf16x4 lds_read_tr(const __bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)p);
+}
+
+__device__ __forceinline__ bf16x8 cat8(bf16x4 lo, bf16x4 hi) {
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// Eight consecutive accumulator registers -> bf16 (round to nearest even).
+__device__ __forceinline__ bf16x8 to_bf16x8(const floatx16& v, int base) {
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = (__bf16)v[base + j];
+  return r;
+}
+
+// LDS tile layout: row-major tiles of `D` bf16 per row, split into 16-byte chunks whose
+// index is XOR-swizzled by the row. The same tile may be read two ways:
+//  - row fragments (ds_read_b128): 8 consecutive rows, one logical chunk -> the swizzle
+//    maps them to 8 distinct bank groups;
+//  - transpose reads: 4 consecutive rows (4-aligned), 2 adjacent chunks -> 8 distinct
+//    bank groups as well.
+__device__ __forceinline__ int swz(int row) { return ((row & 3) << 1) | ((row >> 2) & 1); }
+
+// Element offset of (row, col) in a swizzled tile of D columns; col % 4 == 0.
+template <int D>
+__device__ __forceinline__ int tile_off(int row, int col) {
+  return row * D + (((col >> 3) ^ swz(row)) << 3) + (col & 7);
+}
+
+}  // namespace sra

@@ -1,0 +1,68 @@
+// Kernel argument blocks and launchers (host <-> device interface inside libsra).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sra_config.h"
+
+namespace sra {
+
+// Streams are indexed 0 = generation, 1 = reference.
+struct FwdArgs {
+  const WorkItem* items;
+  const Span* spans;
+  const __bf16* q[2];
+  const __bf16* k[2];
+  const __bf16* v[2];
+  int64_t in_stride[2];  // q/k/v token stride (elements) per stream
+  __bf16* o[2];          // dense [rows, heads, D]
+  float* lse[2];         // [heads, rows]
+  int32_t rows[2];       // packed rows per stream
+  int32_t heads;
+  float scale_log2;      // softmax scale * log2(e)
+};
+
+struct BwdArgs {
+  const WorkItem* items;
+  const Span* spans;
+  const __bf16* q[2];
+  const __bf16* k[2];
+  const __bf16* v[2];
+  int64_t in_stride[2];
+  const __bf16* dout[2];  // dense
+  const float* lse[2];    // [heads, rows], natural log
+  const float* delta[2];  // [heads, rows], rowsum(dO * O)
+  __bf16* dq[2];
+  __bf16* dk[2];
+  __bf16* dv[2];
+  int32_t rows[2];
+  int32_t heads;
+  float scale;            // softmax scale
+  float scale_log2;
+};
+
+struct DeltaArgs {
+  const __bf16* o[2];
+  const __bf16* dout[2];
+  float* delta[2];
+  int32_t rows[2];
+  int32_t heads;
+};
+
+struct FillArgs {
+  const FillRange* ranges;
+  int32_t n_ranges;
+  int32_t heads;
+  int32_t head_dim;
+  __bf16* t[3];      // dense [rows, heads, D] tensors of the range's stream to zero (may be null)
+  float* lse;        // [heads, lse_rows] to set to -inf (may be null)
+  int32_t lse_rows;
+};
+
+hipError_t launch_forward(const FwdArgs& a, int n_items, int head_dim, hipStream_t stream);
+hipError_t launch_delta(const DeltaArgs& a, int head_dim, hipStream_t stream);
+hipError_t launch_dq(const BwdArgs& a, int n_items, int head_dim, hipStream_t stream);
+hipError_t launch_dkv(const BwdArgs& a, int n_items, int head_dim, hipStream_t stream);
+hipError_t launch_fill(const FillArgs& a, hipStream_t stream);
+
+}  // namespace sra

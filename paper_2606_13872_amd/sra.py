@@ -1,0 +1,283 @@
+"""Python binding of libsra (include/sra.h): argument marshalling only.
+
+Every step of Sparse Reference Attention runs in the HIP library; this module turns torch
+tensors into pointers, sizes and the current HIP stream, allocates outputs/workspace with
+torch, and maps status codes to exceptions. It fails loudly if the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import re
+from typing import Dict, Optional, Sequence, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsra.so")
+HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "sra.h")
+
+SRA_OK = 0
+SRA_ERR_INVALID_ARGUMENT = 1
+SRA_ERR_UNSUPPORTED = 2
+SRA_ERR_WORKSPACE_TOO_SMALL = 3
+SRA_ERR_HIP = 4
+SRA_ERR_INTERNAL = 5
+
+SCHED_FORWARD = 0
+SCHED_BWD_DQ = 1
+SCHED_BWD_DKDV = 2
+
+
+class SRAError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{status_string(status)}: {message}")
+        self.status = status
+
+
+class _SampleGeom(ctypes.Structure):
+    _fields_ = [
+        ("gen_frames", ctypes.c_int32), ("gen_h", ctypes.c_int32), ("gen_w", ctypes.c_int32),
+        ("ref_frames", ctypes.c_int32), ("ref_h", ctypes.c_int32), ("ref_w", ctypes.c_int32),
+        ("group_frames", ctypes.c_int32), ("ref_frame_valid", ctypes.c_void_p),
+    ]
+
+
+class _Problem(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32), ("num_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("softmax_scale", ctypes.c_float), ("samples", ctypes.POINTER(_SampleGeom)),
+        ("gen_token_stride", ctypes.c_int64), ("ref_token_stride", ctypes.c_int64),
+        ("flags", ctypes.c_uint32),
+    ]
+
+
+_lib_handle = None
+
+
+def lib() -> ctypes.CDLL:
+    """Loads libsra.so from this package directory (raises if it was not built)."""
+    global _lib_handle
+    if _lib_handle is not None:
+        return _lib_handle
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libsra.so is not built ({LIB_PATH}); run `python -m paper_2606_13872_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER(_Problem)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    sig = {
+        "sra_workspace_size": [P, ctypes.c_int, ctypes.POINTER(sz)],
+        "sra_forward": [P] + [vp] * 6 + [vp, vp, vp, vp] + [vp, sz, vp],
+        "sra_backward": [P] + [vp] * 6 + [vp, vp, vp, vp, vp, vp] + [vp] * 6 + [vp, sz, vp],
+        "sra_pair_counts": [P, ctypes.POINTER(i64), ctypes.POINTER(i64)],
+        "sra_schedule_info": [P, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)],
+        "sra_schedule_mask": [P, ctypes.c_int, i32, vp],
+        "sra_schedule_export": [P, ctypes.c_int, vp, i64, vp, i64],
+        "sra_release_caches": [],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    L.sra_status_string.argtypes = [ctypes.c_int]
+    L.sra_status_string.restype = ctypes.c_char_p
+    L.sra_last_error.argtypes = []
+    L.sra_last_error.restype = ctypes.c_char_p
+    L.sra_version.argtypes = []
+    L.sra_version.restype = ctypes.c_int32
+    _lib_handle = L
+    return L
+
+
+def status_string(status: int) -> str:
+    try:
+        return lib().sra_status_string(status).decode()
+    except ImportError:
+        return f"status {status}"
+
+
+def _check(status: int) -> None:
+    if status != SRA_OK:
+        raise SRAError(status, lib().sra_last_error().decode())
+
+
+def header_functions() -> list:
+    """Names of the functions include/sra.h declares."""
+    text = open(HEADER_PATH).read()
+    return sorted(set(re.findall(r"^(?:sra_status|const char\*|int32_t)\s+(sra_\w+)\s*\(", text, re.M)))
+
+
+class Problem:
+    """A sra_problem built from per-sample geometry objects (attributes as in SampleGeom)."""
+
+    def __init__(self, samples: Sequence, heads: int, head_dim: int, scale: Optional[float] = None,
+                 gen_token_stride: int = 0, ref_token_stride: int = 0, flags: int = 0):
+        self.samples = list(samples)
+        self._geoms = (_SampleGeom * max(1, len(self.samples)))()
+        self._valid = []
+        for i, g in enumerate(self.samples):
+            v = getattr(g, "frame_valid", None)
+            ptr = None
+            if v is not None:
+                buf = (ctypes.c_uint8 * max(1, len(v)))(*[1 if x else 0 for x in v])
+                self._valid.append(buf)
+                ptr = ctypes.cast(buf, ctypes.c_void_p)
+            self._geoms[i] = _SampleGeom(g.gen_frames, g.gen_h, g.gen_w, g.ref_frames, g.ref_h, g.ref_w,
+                                         getattr(g, "group_frames", 1), ptr)
+        self.c = _Problem(len(self.samples), heads, head_dim, 0.0 if scale is None else float(scale),
+                          ctypes.cast(self._geoms, ctypes.POINTER(_SampleGeom)),
+                          gen_token_stride, ref_token_stride, flags)
+        self.heads, self.head_dim = heads, head_dim
+        self.n_gen = sum(g.gen_frames * g.gen_h * g.gen_w for g in self.samples)
+        self.n_ref = sum(g.ref_frames * g.ref_h * g.ref_w for g in self.samples)
+
+    @property
+    def ptr(self):
+        return ctypes.byref(self.c)
+
+    def workspace_size(self, backward: bool) -> int:
+        n = ctypes.c_size_t(0)
+        _check(lib().sra_workspace_size(self.ptr, 1 if backward else 0, ctypes.byref(n)))
+        return int(n.value)
+
+
+# ----------------------------------------------------------------------------- host hooks
+def pair_counts(samples, heads=1, head_dim=128) -> Tuple[int, int]:
+    p = Problem(samples, heads, head_dim)
+    g, r = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(lib().sra_pair_counts(p.ptr, ctypes.byref(g), ctypes.byref(r)))
+    return int(g.value), int(r.value)
+
+
+def schedule_info(samples, which: int, heads=1, head_dim=128) -> Tuple[int, int, int]:
+    p = Problem(samples, heads, head_dim)
+    a, b, c = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(lib().sra_schedule_info(p.ptr, which, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
+    return int(a.value), int(b.value), int(c.value)
+
+
+def schedule_mask(samples, which: int, sample: int, heads=1, head_dim=128):
+    import numpy as np
+
+    p = Problem(samples, heads, head_dim)
+    g = p.samples[sample]
+    n = g.gen_frames * g.gen_h * g.gen_w + g.ref_frames * g.ref_h * g.ref_w
+    out = np.zeros((n, n), dtype=np.uint8)
+    _check(lib().sra_schedule_mask(p.ptr, which, sample, out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def schedule_export(samples, which: int, heads=1, head_dim=128):
+    import numpy as np
+
+    n_items, n_spans, _ = schedule_info(samples, which, heads, head_dim)
+    p = Problem(samples, heads, head_dim)
+    items = np.zeros((n_items, 8), dtype=np.int32)
+    spans = np.zeros((n_spans, 4), dtype=np.int32)
+    _check(lib().sra_schedule_export(p.ptr, which, items.ctypes.data_as(ctypes.c_void_p), items.size,
+                                     spans.ctypes.data_as(ctypes.c_void_p), spans.size))
+    return items, spans
+
+
+def release_caches() -> None:
+    _check(lib().sra_release_caches())
+
+
+# ----------------------------------------------------------------------------- device calls
+def _stream_ptr(device):
+    import torch
+
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None and t.numel() > 0 else ctypes.c_void_p(0)
+
+
+def _token_stride(ts, name):
+    s0 = None
+    for t in ts:
+        if t is None or t.numel() == 0:
+            continue
+        if t.dim() != 3 or t.stride(2) != 1 or t.stride(1) != t.shape[2]:
+            raise ValueError(f"{name}: tensors must be [tokens, heads, head_dim] with contiguous heads")
+        if s0 is None:
+            s0 = t.stride(0)
+        elif t.stride(0) != s0:
+            raise ValueError(f"{name}: q, k and v must share one token stride")
+    return 0 if s0 is None else int(s0)
+
+
+def _alloc_workspace(nbytes, device):
+    import torch
+
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[float] = None,
+            out: Optional[Dict] = None):
+    """SRA forward on the GPU. Returns (o_gen, o_ref, lse_gen, lse_ref)."""
+    import torch
+
+    H, d = q_gen.shape[1], q_gen.shape[2]
+    dev = q_gen.device
+    p = Problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
+                _token_stride([q_ref, k_ref, v_ref], "ref"))
+    for t in (q_gen, k_gen, v_gen, q_ref, k_ref, v_ref):
+        if t is not None and t.dtype != torch.bfloat16:
+            raise TypeError("q/k/v must be bfloat16")
+    if q_gen.shape[0] != p.n_gen or (q_ref is not None and q_ref.shape[0] != p.n_ref):
+        raise ValueError("token counts do not match the geometry")
+    out = out or {}
+    o_gen = out.get("o_gen", torch.empty((p.n_gen, H, d), dtype=torch.bfloat16, device=dev))
+    o_ref = out.get("o_ref", torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
+    lse_gen = out.get("lse_gen", torch.empty((H, p.n_gen), dtype=torch.float32, device=dev))
+    lse_ref = out.get("lse_ref", torch.empty((H, p.n_ref), dtype=torch.float32, device=dev))
+    nbytes = p.workspace_size(False)
+    ws = out.get("workspace")
+    if ws is None or ws.numel() < nbytes:
+        ws = _alloc_workspace(nbytes, dev)
+    _check(lib().sra_forward(p.ptr, _ptr(q_gen), _ptr(k_gen), _ptr(v_gen), _ptr(q_ref), _ptr(k_ref),
+                             _ptr(v_ref), _ptr(o_gen), _ptr(o_ref), _ptr(lse_gen), _ptr(lse_ref),
+                             _ptr(ws), ctypes.c_size_t(ws.numel()), _stream_ptr(dev)))
+    return o_gen, o_ref, lse_gen, lse_ref
+
+
+def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, lse_ref, do_gen, do_ref,
+             samples, scale: Optional[float] = None, out: Optional[Dict] = None):
+    """SRA backward on the GPU. Returns dict dq_gen, dk_gen, dv_gen, dq_ref, dk_ref, dv_ref."""
+    import torch
+
+    H, d = q_gen.shape[1], q_gen.shape[2]
+    dev = q_gen.device
+    p = Problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
+                _token_stride([q_ref, k_ref, v_ref], "ref"))
+    for t in (o_gen, o_ref, do_gen, do_ref):
+        if t is not None and t.numel() and not t.is_contiguous():
+            raise ValueError("o and do must be dense [tokens, heads, head_dim]")
+    out = out or {}
+    g = {}
+    for n in ("dq_gen", "dk_gen", "dv_gen"):
+        g[n] = out.get(n, torch.empty((p.n_gen, H, d), dtype=torch.bfloat16, device=dev))
+    for n in ("dq_ref", "dk_ref", "dv_ref"):
+        g[n] = out.get(n, torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
+    nbytes = p.workspace_size(True)
+    ws = out.get("workspace")
+    if ws is None or ws.numel() < nbytes:
+        ws = _alloc_workspace(nbytes, dev)
+    _check(lib().sra_backward(p.ptr, _ptr(q_gen), _ptr(k_gen), _ptr(v_gen), _ptr(q_ref), _ptr(k_ref),
+                              _ptr(v_ref), _ptr(o_gen), _ptr(o_ref), _ptr(lse_gen), _ptr(lse_ref),
+                              _ptr(do_gen), _ptr(do_ref), _ptr(g["dq_gen"]), _ptr(g["dk_gen"]),
+                              _ptr(g["dv_gen"]), _ptr(g["dq_ref"]), _ptr(g["dk_ref"]), _ptr(g["dv_ref"]),
+                              _ptr(ws), ctypes.c_size_t(ws.numel()), _stream_ptr(dev)))
+    return g
+
+
+def useful_flops(samples, heads: int, head_dim: int) -> Tuple[int, int]:
+    """Useful FLOP of one forward and one backward call: 4 d and 10 d per visible pair per head."""
+    gp, rp = pair_counts(samples, heads, head_dim)
+    pairs = (gp + rp) * heads
+    return 4 * head_dim * pairs, 10 * head_dim * pairs
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

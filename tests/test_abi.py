@@ -1,0 +1,95 @@
+"""The C-ABI library loads, exports what include/sra.h declares, and validates on the host.
+
+No device work happens here: every call either fails validation before anything is
+enqueued or is a host-only hook.
+"""
+import ctypes
+
+import pytest
+
+from paper_2606_13872_amd import sra
+from sra_inputs import SampleGeom
+
+
+def test_library_exports_every_declared_function():
+    names = sra.header_functions()
+    assert set(names) >= {"sra_workspace_size", "sra_forward", "sra_backward", "sra_pair_counts",
+                          "sra_schedule_info", "sra_schedule_mask", "sra_schedule_export",
+                          "sra_release_caches", "sra_status_string", "sra_last_error", "sra_version"}
+    L = sra.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.sra_version() >= 100
+    assert sra.status_string(0) == "SRA_OK"
+    assert sra.status_string(3) == "SRA_ERR_WORKSPACE_TOO_SMALL"
+
+
+GOOD = [SampleGeom(2, 8, 8, 4, 8, 8)]
+
+
+@pytest.mark.parametrize("samples,heads,d,stride,status", [
+    ([SampleGeom(0, 8, 8, 4, 8, 8)], 1, 64, 0, sra.SRA_ERR_INVALID_ARGUMENT),
+    ([SampleGeom(2, 8, 8, -1, 8, 8)], 1, 64, 0, sra.SRA_ERR_INVALID_ARGUMENT),
+    ([SampleGeom(2, 8, 8, 4, 8, 8, group_frames=0)], 1, 64, 0, sra.SRA_ERR_INVALID_ARGUMENT),
+    ([SampleGeom(2, 8, 8, 2, 0, 8)], 1, 64, 0, sra.SRA_ERR_INVALID_ARGUMENT),
+    (GOOD, 0, 64, 0, sra.SRA_ERR_INVALID_ARGUMENT),
+    (GOOD, 1, 96, 0, sra.SRA_ERR_UNSUPPORTED),
+    (GOOD, 1, 0, 0, sra.SRA_ERR_INVALID_ARGUMENT),
+    (GOOD, 2, 64, 64, sra.SRA_ERR_INVALID_ARGUMENT),      # stride < H*d
+    (GOOD, 2, 64, 132, sra.SRA_ERR_INVALID_ARGUMENT),     # stride not a multiple of 8
+    ([SampleGeom(70000, 200, 200, 0, 1, 1)], 1, 64, 0, sra.SRA_ERR_INVALID_ARGUMENT),  # > int32 rows
+])
+def test_invalid_problems_are_rejected(samples, heads, d, stride, status):
+    p = sra.Problem(samples, heads, d, gen_token_stride=stride)
+    n = ctypes.c_size_t(0)
+    st = sra.lib().sra_workspace_size(p.ptr, 0, ctypes.byref(n))
+    assert st == status
+    assert len(sra.lib().sra_last_error()) > 0
+
+
+def test_flags_and_batch_validation():
+    p = sra.Problem(GOOD, 1, 64, flags=1)
+    with pytest.raises(sra.SRAError) as e:
+        p.workspace_size(False)
+    assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+    p = sra.Problem([], 1, 64)
+    with pytest.raises(sra.SRAError):
+        p.workspace_size(False)
+
+
+def test_workspace_size_is_host_only_and_grows_for_backward():
+    p = sra.Problem(GOOD, 1, 64)
+    f, b = p.workspace_size(False), p.workspace_size(True)
+    assert f > 0 and b > f and f % 256 == 0 and b % 256 == 0
+
+
+def test_forward_rejects_null_and_unaligned_pointers_before_any_launch():
+    p = sra.Problem(GOOD, 1, 64)
+    L = sra.lib()
+    fake = ctypes.c_void_p(1 << 20)
+    null = ctypes.c_void_p(0)
+    args = [fake] * 6 + [fake, fake, fake, fake]
+    # null gen pointer
+    st = L.sra_forward(p.ptr, null, *args[1:], fake, ctypes.c_size_t(1 << 20), null)
+    assert st == sra.SRA_ERR_INVALID_ARGUMENT
+    # unaligned pointer
+    st = L.sra_forward(p.ptr, ctypes.c_void_p((1 << 20) + 2), *args[1:], fake, ctypes.c_size_t(1 << 20), null)
+    assert st == sra.SRA_ERR_INVALID_ARGUMENT
+    # workspace too small
+    st = L.sra_forward(p.ptr, *args, fake, ctypes.c_size_t(16), null)
+    assert st == sra.SRA_ERR_WORKSPACE_TOO_SMALL
+    # workspace misaligned
+    st = L.sra_forward(p.ptr, *args, ctypes.c_void_p((1 << 20) + 16), ctypes.c_size_t(1 << 20), null)
+    assert st == sra.SRA_ERR_INVALID_ARGUMENT
+    # reference pointers may be NULL only when there is no reference
+    ref_null = [fake] * 3 + [null] * 3 + [fake, null, fake, null]
+    st = L.sra_forward(p.ptr, *ref_null, fake, ctypes.c_size_t(1 << 20), null)
+    assert st == sra.SRA_ERR_INVALID_ARGUMENT
+
+
+def test_backward_rejects_small_workspace():
+    p = sra.Problem(GOOD, 1, 64)
+    fake = ctypes.c_void_p(1 << 20)
+    st = sra.lib().sra_backward(p.ptr, *([fake] * 18), fake, ctypes.c_size_t(p.workspace_size(True) - 256),
+                                ctypes.c_void_p(0))
+    assert st == sra.SRA_ERR_WORKSPACE_TOO_SMALL

@@ -1,0 +1,270 @@
+"""GPU (libsra HIP kernels through the C ABI) vs the CPU oracle, element by element.
+
+Bar: max |err| <= 1e-2 and mean |err| <= 1e-3 on O, dQ, dK, dV (bf16 out, fp32 accumulate);
+log-sum-exp max |err| <= 1e-3; relative L2 error per (stream, head) <= 1e-2. The oracle runs
+in float64 on the exact values of the bf16 inputs (the fp32 oracle meets the same bar).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_13872_amd import sra
+from sra_inputs import SampleGeom, make_inputs, to_numpy64
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS, MEAN_ABS, REL, LSE_ABS = 1e-2, 1e-3, 1e-2, 1e-3
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def assert_close(name, got, want, heads_axis):
+    g = _np(got) if isinstance(got, torch.Tensor) else got
+    assert g.shape == want.shape, (name, g.shape, want.shape)
+    if want.size == 0:
+        return
+    d = np.abs(g - want)
+    assert np.all(np.isfinite(g)), f"{name}: non-finite output"
+    assert d.max() <= MAX_ABS, f"{name}: max abs err {d.max():.3e}"
+    assert d.mean() <= MEAN_ABS, f"{name}: mean abs err {d.mean():.3e}"
+    gm = np.moveaxis(g, heads_axis, 0).reshape(g.shape[heads_axis], -1)
+    wm = np.moveaxis(want, heads_axis, 0).reshape(want.shape[heads_axis], -1)
+    for h in range(gm.shape[0]):
+        nw = np.linalg.norm(wm[h])
+        if nw == 0:
+            assert np.all(gm[h] == 0), f"{name}: head {h} should be exactly 0"
+        else:
+            rel = np.linalg.norm(gm[h] - wm[h]) / nw
+            assert rel <= REL, f"{name}: head {h} relative err {rel:.3e}"
+
+
+def assert_lse(name, got, want):
+    g = _np(got)
+    inf_w = np.isneginf(want)
+    assert np.array_equal(np.isneginf(g), inf_w), f"{name}: -inf pattern differs"
+    if (~inf_w).any():
+        err = np.abs(g[~inf_w] - want[~inf_w]).max()
+        assert err <= LSE_ABS, f"{name}: lse max err {err:.3e}"
+
+
+def run_gpu(x, samples, scale=None, backward=True):
+    dev = torch.device("cuda")
+    y = {k: v.to(dev) for k, v in x.items()}
+    o_gen, o_ref, lse_gen, lse_ref = sra.forward(y["q_gen"], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"],
+                                                 y["v_ref"], samples, scale)
+    out = {"o_gen": o_gen, "o_ref": o_ref, "lse_gen": lse_gen, "lse_ref": lse_ref}
+    if backward:
+        out.update(sra.backward(y["q_gen"], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"],
+                                o_gen, o_ref, lse_gen, lse_ref, y["do_gen"], y["do_ref"], samples, scale))
+    torch.cuda.synchronize()
+    return out
+
+
+def check_against_oracle(samples, H, d, seed, rms=False, scale=None, backward=True):
+    x = make_inputs(samples, H, d, seed, rms_norm_qk=rms)
+    got = run_gpu(x, samples, scale, backward)
+    xo = {k: to_numpy64(v) for k, v in x.items()}
+    if backward:
+        want = oracle.sra_backward(xo, samples, scale)
+    else:
+        o_gen, o_ref, lse_gen, lse_ref = oracle.sra_forward(xo, samples, scale)
+        want = {"o_gen": o_gen, "o_ref": o_ref, "lse_gen": lse_gen, "lse_ref": lse_ref}
+    for n in ("o_gen", "o_ref"):
+        assert_close(n, got[n], want[n], 1)
+    assert_lse("lse_gen", got["lse_gen"], want["lse_gen"])
+    assert_lse("lse_ref", got["lse_ref"], want["lse_ref"])
+    if backward:
+        for n in ("dq_gen", "dk_gen", "dv_gen", "dq_ref", "dk_ref", "dv_ref"):
+            assert_close(n, got[n], want[n], 1)
+    return x, got
+
+
+CASES = {
+    # name: (samples, H, d, seed, rms)
+    "tiny": ([SampleGeom(2, 8, 8, 4, 8, 8)], 1, 64, 0, False),
+    "multi_tile_ragged": ([SampleGeom(2, 20, 20, 3, 13, 11)], 3, 128, 11, False),
+    "multi_tile_rms": ([SampleGeom(3, 16, 13, 2, 16, 13)], 2, 128, 12, True),
+    "invalid_frames": ([SampleGeom(1, 16, 20, 6, 5, 7, frame_valid=[1, 0, 1, 1, 0, 1])], 2, 128, 13, False),
+    "groups_of_two": ([SampleGeom(1, 16, 20, 6, 5, 7, group_frames=2, frame_valid=[1, 0, 1, 1, 0, 0])], 2, 128, 14, False),
+    "whole_ref_group": ([SampleGeom(1, 10, 10, 4, 9, 9, group_frames=4)], 1, 128, 15, False),
+    "no_reference": ([SampleGeom(3, 10, 10, 0, 1, 1)], 2, 128, 16, False),
+    "all_ref_invalid": ([SampleGeom(1, 12, 12, 3, 6, 6, frame_valid=[0, 0, 0])], 1, 128, 17, False),
+    "varlen": ([SampleGeom(2, 9, 15, 2, 9, 15), SampleGeom(1, 11, 7, 5, 6, 6), SampleGeom(1, 5, 5, 0, 3, 3),
+                SampleGeom(2, 8, 8, 3, 8, 8, group_frames=3, frame_valid=[1, 1, 0])], 2, 128, 18, True),
+    "d64_multi_tile": ([SampleGeom(2, 18, 18, 3, 12, 12)], 2, 64, 19, False),
+    "d64_invalid_groups": ([SampleGeom(1, 9, 9, 5, 7, 5, group_frames=2, frame_valid=[1, 1, 0, 1, 1])], 2, 64, 20, True),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_forward_backward_parity(case):
+    samples, H, d, seed, rms = CASES[case]
+    print(f"[parity] {case}", flush=True)
+    check_against_oracle(samples, H, d, seed, rms)
+
+
+def test_custom_scale():
+    check_against_oracle([SampleGeom(1, 8, 16, 2, 8, 8)], 2, 128, 21, scale=0.05)
+
+
+def test_sharp_scale_relative_error():
+    """At scale 0.2 gradients reach O(1), where bf16 rounding alone exceeds 1e-2 absolute:
+    only the relative L2 bar applies."""
+    samples, H, d = [SampleGeom(1, 8, 16, 2, 8, 8)], 2, 128
+    x = make_inputs(samples, H, d, 21)
+    got = run_gpu(x, samples, 0.2)
+    want = oracle.sra_backward({k: to_numpy64(v) for k, v in x.items()}, samples, 0.2)
+    for n in ("o_gen", "o_ref", "dq_gen", "dk_gen", "dv_gen", "dq_ref", "dk_ref", "dv_ref"):
+        g, w = _np(got[n]), want[n]
+        for h in range(H):
+            rel = np.linalg.norm(g[:, h] - w[:, h]) / np.linalg.norm(w[:, h])
+            assert rel <= REL, (n, h, rel)
+
+
+def test_fp32_oracle_meets_the_same_bar():
+    samples, H, d = [SampleGeom(2, 12, 12, 3, 8, 9)], 2, 128
+    x = make_inputs(samples, H, d, 22)
+    got = run_gpu(x, samples)
+    xo = {k: to_numpy64(v).astype(np.float32) for k, v in x.items()}
+    w = oracle.sra_backward(xo, samples, dtype=np.float32)
+    for n in ("o_gen", "o_ref", "dq_gen", "dk_gen", "dv_gen", "dq_ref", "dk_ref", "dv_ref"):
+        assert_close(n, got[n], w[n].astype(np.float64), 1)
+
+
+def test_strided_qkv_packed_inputs():
+    """q, k, v as views of one [tokens, 3, H, d] buffer (token stride 3*H*d)."""
+    samples, H, d = [SampleGeom(2, 10, 12, 3, 7, 9)], 2, 128
+    x = make_inputs(samples, H, d, 23)
+    dev = torch.device("cuda")
+    packed = {}
+    for s in ("gen", "ref"):
+        buf = torch.stack([x[f"q_{s}"], x[f"k_{s}"], x[f"v_{s}"]], dim=1).to(dev)
+        packed[s] = buf
+    o_gen, o_ref, lse_gen, lse_ref = sra.forward(packed["gen"][:, 0], packed["gen"][:, 1], packed["gen"][:, 2],
+                                                 packed["ref"][:, 0], packed["ref"][:, 1], packed["ref"][:, 2], samples)
+    g = sra.backward(packed["gen"][:, 0], packed["gen"][:, 1], packed["gen"][:, 2], packed["ref"][:, 0],
+                     packed["ref"][:, 1], packed["ref"][:, 2], o_gen, o_ref, lse_gen, lse_ref,
+                     x["do_gen"].to(dev), x["do_ref"].to(dev), samples)
+    ref = run_gpu(x, samples)
+    for n, t in (("o_gen", o_gen), ("o_ref", o_ref), ("lse_gen", lse_gen), ("lse_ref", lse_ref)):
+        assert torch.equal(t, ref[n]), n
+    for n in g:
+        assert torch.equal(g[n], ref[n]), n
+
+
+# ------------------------------------------------------------------------------ properties
+def test_asymmetry_is_bitwise_on_gpu():
+    """Fresh gen inputs leave reference outputs, LSE and dQ_ref bitwise unchanged."""
+    samples, H, d = [SampleGeom(2, 16, 16, 3, 9, 10)], 2, 128
+    x = make_inputs(samples, H, d, 24)
+    a = run_gpu(x, samples)
+    y = dict(x)
+    z = make_inputs(samples, H, d, 99)
+    for n in ("q_gen", "k_gen", "v_gen", "do_gen"):
+        y[n] = z[n]
+    b = run_gpu(y, samples)
+    for n in ("o_ref", "lse_ref", "dq_ref"):
+        assert torch.equal(a[n], b[n]), n
+
+
+def test_zero_keys_count_law_on_gpu():
+    """K = 0: LSE_q = ln |visible keys of q| (closed form per row) on the GPU."""
+    g = SampleGeom(1, 12, 20, 5, 6, 7, group_frames=2, frame_valid=[1, 1, 0, 1, 1])
+    H, d = 2, 128
+    x = make_inputs([g], H, d, 25)
+    x["k_gen"].zero_()
+    x["k_ref"].zero_()
+    got = run_gpu(x, [g], backward=False)
+    F = g.ref_h * g.ref_w
+    v = g.frame_valid
+    n_gen = g.n_gen + F * sum(v)
+    lg = _np(got["lse_gen"])
+    assert np.abs(lg - math.log(n_gen)).max() < 1e-5
+    lr = _np(got["lse_ref"])
+    for f in range(g.ref_frames):
+        grp = f // g.group_frames
+        cnt = F * sum(v[grp * g.group_frames:(grp + 1) * g.group_frames])
+        seg = lr[:, f * F:(f + 1) * F]
+        if v[f]:
+            assert np.abs(seg - math.log(cnt)).max() < 1e-5
+            assert np.all(np.round(np.exp(seg)) == cnt)
+        else:
+            assert np.all(np.isneginf(seg))
+
+
+def test_run_to_run_determinism():
+    samples, H, d = [SampleGeom(2, 16, 16, 3, 9, 10)], 2, 128
+    x = make_inputs(samples, H, d, 26)
+    a = run_gpu(x, samples)
+    b = run_gpu(x, samples)
+    for n in a:
+        assert torch.equal(a[n], b[n]), n
+
+
+def test_canary_guard_bands_untouched():
+    """Outputs live inside larger buffers filled with a sentinel; nothing outside is written."""
+    samples, H, d = [SampleGeom(1, 20, 13, 3, 11, 7, frame_valid=[1, 0, 1])], 2, 128
+    x = make_inputs(samples, H, d, 27)
+    dev = torch.device("cuda")
+    y = {k: v.to(dev) for k, v in x.items()}
+    pad = 4096
+    sentinel = -1032.0  # exact in bf16 and fp32
+
+    def guarded(shape, dtype):
+        n = int(np.prod(shape))
+        buf = torch.full((n + 2 * pad,), sentinel, dtype=dtype, device=dev)
+        return buf, buf[pad:pad + n].view(shape)
+
+    bufs, out = {}, {}
+    for n, shape, dt in (("o_gen", y["q_gen"].shape, torch.bfloat16), ("o_ref", y["q_ref"].shape, torch.bfloat16),
+                         ("lse_gen", (H, g_rows := y["q_gen"].shape[0]), torch.float32),
+                         ("lse_ref", (H, y["q_ref"].shape[0]), torch.float32)):
+        bufs[n], out[n] = guarded(shape, dt)
+    sra.forward(y["q_gen"], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], samples, out=out)
+    gout = {}
+    for n in ("dq_gen", "dk_gen", "dv_gen"):
+        bufs[n], gout[n] = guarded(y["q_gen"].shape, torch.bfloat16)
+    for n in ("dq_ref", "dk_ref", "dv_ref"):
+        bufs[n], gout[n] = guarded(y["q_ref"].shape, torch.bfloat16)
+    sra.backward(y["q_gen"], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], out["o_gen"], out["o_ref"],
+                 out["lse_gen"], out["lse_ref"], y["do_gen"], y["do_ref"], samples, out=gout)
+    torch.cuda.synchronize()
+    for n, b in bufs.items():
+        assert torch.all(b[:pad].float() == sentinel), n
+        assert torch.all(b[-pad:].float() == sentinel), n
+    ref = run_gpu(x, samples)
+    for n in out:
+        assert torch.equal(out[n], ref[n]), n
+    for n in gout:
+        assert torch.equal(gout[n], ref[n]), n
+
+
+def test_error_paths_do_not_launch():
+    """A rejected call leaves its outputs untouched."""
+    samples, H, d = [SampleGeom(1, 8, 8, 2, 8, 8)], 1, 128
+    x = make_inputs(samples, H, d, 28)
+    dev = torch.device("cuda")
+    y = {k: v.to(dev) for k, v in x.items()}
+    o = {"o_gen": torch.full((64, 1, 128), 7.0, dtype=torch.bfloat16, device=dev),
+         "workspace": torch.empty(16, dtype=torch.uint8, device=dev)}
+    with pytest.raises(sra.SRAError) as e:
+        # workspace too small is only detected if the binding passes the small buffer: call the C ABI
+        p = sra.Problem(samples, H, d)
+        L = sra.lib()
+        import ctypes
+        st = L.sra_forward(p.ptr, *[ctypes.c_void_p(y[n].data_ptr()) for n in
+                                    ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")],
+                           ctypes.c_void_p(o["o_gen"].data_ptr()), ctypes.c_void_p(y["q_ref"].data_ptr()),
+                           ctypes.c_void_p(y["q_gen"].data_ptr()), ctypes.c_void_p(y["q_ref"].data_ptr()),
+                           ctypes.c_void_p(o["workspace"].data_ptr()), ctypes.c_size_t(16), ctypes.c_void_p(0))
+        sra._check(st)
+    assert e.value.status == sra.SRA_ERR_WORKSPACE_TOO_SMALL
+    torch.cuda.synchronize()
+    assert torch.all(o["o_gen"].float() == 7.0)
+    with pytest.raises(ValueError):
+        sra.forward(y["q_gen"][:10], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], samples)

@@ -1,0 +1,119 @@
+"""Host schedules vs the oracle's explicit visibility mask, bit-exact.
+
+The library's three tile schedules (forward, dQ, dK/dV) are expanded through the C ABI
+into per-pair coverage counts; each must equal the oracle's 0/1 mask exactly: every
+visible pair computed once, nothing else computed. Pair counts are checked against the
+closed form and the golden values the oracle wrote.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_13872_amd import sra
+from sra_inputs import SWEEP_POINTS, SampleGeom, workload
+
+SCHEDS = [sra.SCHED_FORWARD, sra.SCHED_BWD_DQ, sra.SCHED_BWD_DKDV]
+
+GEOMS = [
+    [SampleGeom(2, 8, 8, 4, 8, 8)],                                        # tiny workload shape
+    [SampleGeom(1, 3, 5, 0, 1, 1)],                                        # no reference
+    [SampleGeom(3, 7, 11, 5, 6, 9)],                                       # F = 54: ragged tiles
+    [SampleGeom(2, 9, 9, 6, 5, 7, frame_valid=[1, 0, 0, 1, 1, 0])],        # invalid frames
+    [SampleGeom(2, 9, 9, 6, 5, 7, group_frames=2, frame_valid=[1, 0, 1, 1, 0, 0])],
+    [SampleGeom(1, 16, 20, 7, 4, 9, group_frames=3)],                      # groups 3,3,1
+    [SampleGeom(1, 8, 8, 5, 8, 8, group_frames=5)],                        # whole reference
+    [SampleGeom(1, 4, 4, 3, 4, 4, frame_valid=[0, 0, 0])],                 # all reference invalid
+    [SampleGeom(2, 10, 13, 3, 10, 13), SampleGeom(1, 17, 3, 2, 7, 7),      # varlen batch
+     SampleGeom(3, 5, 5, 0, 5, 5), SampleGeom(1, 20, 20, 4, 6, 6, group_frames=2, frame_valid=[1, 1, 0, 1])],
+    [SampleGeom(1, 16, 16, 2, 16, 16, group_frames=1)],                    # tile-aligned sizes
+]
+
+
+@pytest.mark.parametrize("gi", range(len(GEOMS)))
+@pytest.mark.parametrize("which", SCHEDS)
+def test_schedule_mask_is_the_visibility_mask(gi, which):
+    samples = GEOMS[gi]
+    for b, g in enumerate(samples):
+        want = oracle.visibility_mask(g).astype(np.uint8)
+        got = sra.schedule_mask(samples, which, b)
+        assert got.shape == want.shape
+        assert np.array_equal(got, want), (which, b, np.argwhere(got != want)[:5])
+
+
+@pytest.mark.parametrize("gi", range(len(GEOMS)))
+def test_pair_counts_closed_form_equals_mask(gi):
+    samples = GEOMS[gi]
+    assert sra.pair_counts(samples) == oracle.pair_counts(samples)
+    total = sum(oracle.pair_counts(samples))
+    for which in SCHEDS:
+        _, _, covered = sra.schedule_info(samples, which)
+        assert covered == total
+
+
+def _golden():
+    with open(os.path.join(os.path.dirname(__file__), "golden", "pair_counts.json")) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("name", ["tiny", "480p"] + [f"sweep_{n}" for n in SWEEP_POINTS] + ["720p", "varlen"])
+def test_full_size_pair_counts_and_coverage(name):
+    w = workload(name)
+    gold = _golden()[name]
+    gp, rp = sra.pair_counts(w.samples, w.heads, w.head_dim)
+    assert (gp, rp) == (gold["gen_pairs"], gold["ref_pairs"])
+    for which in SCHEDS:
+        _, _, covered = sra.schedule_info(w.samples, which, w.heads, w.head_dim)
+        assert covered == gp + rp
+
+
+def test_survey_quoted_pair_counts():
+    """Hand-derived closed forms G(G+R) + R F for the named workloads."""
+    g = _golden()
+    assert g["tiny"]["gen_pairs"] + g["tiny"]["ref_pairs"] == 128 * 384 + 256 * 64 == 65536
+    assert g["480p"]["gen_pairs"] == 32760 * (32760 + 14040)
+    assert g["720p"]["gen_pairs"] + g["720p"]["ref_pairs"] == 75600 * 151200 + 75600 * 3600
+    assert g["varlen"]["gen_pairs"] + g["varlen"]["ref_pairs"] == 13849804800
+
+
+@pytest.mark.parametrize("which", SCHEDS)
+def test_schedule_tables_are_well_formed(which):
+    samples = GEOMS[8]
+    heads = 8
+    items, spans = sra.schedule_export(samples, which, heads=heads)
+    tile = {sra.SCHED_FORWARD: 256, sra.SCHED_BWD_DQ: 256, sra.SCHED_BWD_DKDV: 128}[which]
+    n_gen = sum(g.n_gen for g in samples)
+    n_ref = sum(g.n_ref for g in samples)
+    rows = (n_gen, n_ref)
+    real = items[items[:, 0] >= 0]
+    assert np.all((real[:, 3] > 0) & (real[:, 3] <= tile))
+    assert np.all(real[:, 1] < heads)
+    for s in (0, 1):
+        sel = real[real[:, 0] == s]
+        assert np.all(sel[:, 2] + sel[:, 3] <= rows[s])
+    assert np.all(spans[:, 2] > 0)
+    for s in (0, 1):
+        sel = spans[spans[:, 0] == s]
+        assert np.all((sel[:, 1] >= 0) & (sel[:, 1] + sel[:, 2] <= rows[s]))
+    assert np.all(real[:, 4] + real[:, 5] <= len(spans))
+    # every (head, row) of every valid row is covered by exactly one tile
+    for s in (0, 1):
+        for h in range(heads):
+            cov = np.zeros(rows[s], dtype=np.int32)
+            for it in real[(real[:, 0] == s) & (real[:, 1] == h)]:
+                cov[it[2]:it[2] + it[3]] += 1
+            assert cov.max() <= 1
+
+
+def test_xcd_order_pins_heads_and_puts_long_items_first():
+    w = workload("480p")
+    items, spans = sra.schedule_export(w.samples, sra.SCHED_FORWARD, w.heads, w.head_dim)
+    assert len(items) % 8 == 0
+    for x in range(8):
+        sub = items[x::8]
+        sub = sub[sub[:, 0] >= 0]
+        assert np.all(sub[:, 1] % 8 == x)
+        cost = np.array([spans[i[4]:i[4] + i[5], 2].sum() for i in sub])
+        assert np.all(np.diff(cost) <= 0)
