@@ -138,6 +138,26 @@ sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, ui
 sra_status sra_schedule_export(const sra_problem* p, int which, int32_t* items,
                                int64_t items_capacity, int32_t* spans, int64_t spans_capacity);
 
+/* ---- per-kernel timing (tracing hook) ---------------------------------------------------- */
+
+/* Kernels of the library, for sra_kernel_timing. */
+enum {
+  SRA_KERNEL_FORWARD = 0,   /* forward pass                              */
+  SRA_KERNEL_DELTA = 1,     /* backward: D = rowsum(dO * O)              */
+  SRA_KERNEL_DKDV = 2,      /* backward: dK and dV (key-major)           */
+  SRA_KERNEL_DQ = 3,        /* backward: dQ (query-major)                */
+  SRA_KERNEL_FILL = 4,      /* rows of invalid reference frames          */
+  SRA_KERNEL_COUNT = 5
+};
+
+/* enable != 0: from now on every kernel launch is bracketed by two hipEvents recorded on the
+ * caller's stream, and the accumulated totals are reset. enable == 0 stops recording. */
+sra_status sra_kernel_timing_enable(int enable);
+
+/* Waits for the recorded events and returns the summed duration (ms) and launch count of
+ * kernel `kernel` (SRA_KERNEL_*) since timing was enabled. */
+sra_status sra_kernel_timing(int kernel, double* total_ms, int64_t* launches);
+
 /* Frees cached schedules and their pinned host buffers, after waiting for the copies that
  * read them. Safe to call at any time; later calls rebuild what they need. */
 sra_status sra_release_caches(void);

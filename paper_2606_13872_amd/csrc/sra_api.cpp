@@ -164,6 +164,85 @@ sra_status hip_fail(hipError_t e, const char* what) {
   return fail(SRA_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
+// Opt-in per-kernel timing: launches are bracketed by events on the launch stream; the
+// elapsed times are collected when read.
+class KernelTimer {
+ public:
+  void enable(bool on) {
+    std::lock_guard<std::mutex> lk(mu_);
+    drain();
+    for (auto& ev : pending_) destroy(ev);
+    pending_.clear();
+    for (int i = 0; i < SRA_KERNEL_COUNT; ++i) total_[i] = 0.0, count_[i] = 0;
+    on_ = on;
+  }
+  bool on() const { return on_; }
+  // Returns an event recorded on `s` (nullptr if timing is off or the event failed).
+  hipEvent_t mark(hipStream_t s) {
+    if (!on_) return nullptr;
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventRecord(e, s) != hipSuccess) {
+      (void)hipEventDestroy(e);
+      return nullptr;
+    }
+    return e;
+  }
+  void add(int kernel, hipEvent_t a, hipEvent_t b) {
+    if (!a || !b) {
+      if (a) (void)hipEventDestroy(a);
+      if (b) (void)hipEventDestroy(b);
+      return;
+    }
+    std::lock_guard<std::mutex> lk(mu_);
+    pending_.push_back({kernel, a, b});
+  }
+  void read(int kernel, double* ms, int64_t* n) {
+    std::lock_guard<std::mutex> lk(mu_);
+    drain();
+    if (ms) *ms = total_[kernel];
+    if (n) *n = count_[kernel];
+  }
+
+ private:
+  struct Ev { int k; hipEvent_t a, b; };
+  static void destroy(Ev& e) {
+    (void)hipEventDestroy(e.a);
+    (void)hipEventDestroy(e.b);
+  }
+  void drain() {
+    for (auto& e : pending_) {
+      float t = 0.f;
+      if (hipEventSynchronize(e.b) == hipSuccess && hipEventElapsedTime(&t, e.a, e.b) == hipSuccess) {
+        total_[e.k] += t;
+        count_[e.k] += 1;
+      }
+      destroy(e);
+    }
+    pending_.clear();
+  }
+  std::mutex mu_;
+  bool on_ = false;
+  std::vector<Ev> pending_;
+  double total_[SRA_KERNEL_COUNT] = {};
+  int64_t count_[SRA_KERNEL_COUNT] = {};
+};
+
+KernelTimer& timer() {
+  static KernelTimer* t = new KernelTimer();
+  return *t;
+}
+
+// Launches `fn` (returning hipError_t) with optional timing under kernel id `k`.
+template <class Fn>
+hipError_t timed(int k, hipStream_t s, Fn&& fn) {
+  hipEvent_t a = timer().mark(s);
+  hipError_t e = fn();
+  hipEvent_t b = timer().mark(s);
+  timer().add(k, a, b);
+  return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -225,7 +304,7 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
   a.rows[1] = int32_t(L.sum_ref);
   a.heads = L.heads;
   a.scale_log2 = float(double(L.scale) * 1.4426950408889634);
-  hipError_t e = launch_forward(a, int(P.fwd.items.size()), L.head_dim, s);
+  hipError_t e = timed(SRA_KERNEL_FORWARD, s, [&] { return launch_forward(a, int(P.fwd.items.size()), L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "forward launch");
   if (!P.fill.empty()) {
     FillArgs f{};
@@ -236,7 +315,7 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
     f.t[0] = static_cast<__bf16*>(o_ref);
     f.lse = lse_ref;
     f.lse_rows = int32_t(L.sum_ref);
-    e = launch_fill(f, s);
+    e = timed(SRA_KERNEL_FILL, s, [&] { return launch_fill(f, s); });
     if (e != hipSuccess) return hip_fail(e, "fill launch");
   }
   return SRA_OK;
@@ -281,7 +360,7 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
   d.rows[0] = int32_t(L.sum_gen);
   d.rows[1] = int32_t(L.sum_ref);
   d.heads = L.heads;
-  e = launch_delta(d, L.head_dim, s);
+  e = timed(SRA_KERNEL_DELTA, s, [&] { return launch_delta(d, L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "delta launch");
 
   const Plan& P = cp->plan;
@@ -314,11 +393,11 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
 
   a.items = reinterpret_cast<const WorkItem*>(ws + cp->bwd.offsets[2]);
   a.spans = reinterpret_cast<const Span*>(ws + cp->bwd.offsets[3]);
-  e = launch_dkv(a, int(P.dkv.items.size()), L.head_dim, s);
+  e = timed(SRA_KERNEL_DKDV, s, [&] { return launch_dkv(a, int(P.dkv.items.size()), L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "dkv launch");
   a.items = reinterpret_cast<const WorkItem*>(ws + cp->bwd.offsets[0]);
   a.spans = reinterpret_cast<const Span*>(ws + cp->bwd.offsets[1]);
-  e = launch_dq(a, int(P.dq.items.size()), L.head_dim, s);
+  e = timed(SRA_KERNEL_DQ, s, [&] { return launch_dq(a, int(P.dq.items.size()), L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "dq launch");
   if (!P.fill.empty()) {
     FillArgs f{};
@@ -329,7 +408,7 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
     f.t[0] = static_cast<__bf16*>(dq_ref);
     f.t[1] = static_cast<__bf16*>(dk_ref);
     f.t[2] = static_cast<__bf16*>(dv_ref);
-    e = launch_fill(f, s);
+    e = timed(SRA_KERNEL_FILL, s, [&] { return launch_fill(f, s); });
     if (e != hipSuccess) return hip_fail(e, "fill launch");
   }
   return SRA_OK;
@@ -428,6 +507,19 @@ sra_status sra_schedule_export(const sra_problem* p, int which, int32_t* items, 
     if (spans_capacity < int64_t(S->spans.size()) * 4) return fail(SRA_ERR_INVALID_ARGUMENT, "spans buffer too small");
     std::memcpy(spans, S->spans.data(), S->spans.size() * sizeof(Span));
   }
+  return SRA_OK;
+}
+
+sra_status sra_kernel_timing_enable(int enable) {
+  g_last_error.clear();
+  timer().enable(enable != 0);
+  return SRA_OK;
+}
+
+sra_status sra_kernel_timing(int kernel, double* total_ms, int64_t* launches) {
+  g_last_error.clear();
+  if (kernel < 0 || kernel >= SRA_KERNEL_COUNT) return fail(SRA_ERR_INVALID_ARGUMENT, "unknown kernel id");
+  timer().read(kernel, total_ms, launches);
   return SRA_OK;
 }
 

@@ -73,6 +73,8 @@ def lib() -> ctypes.CDLL:
         "sra_schedule_mask": [P, ctypes.c_int, i32, vp],
         "sra_schedule_export": [P, ctypes.c_int, vp, i64, vp, i64],
         "sra_release_caches": [],
+        "sra_kernel_timing_enable": [ctypes.c_int],
+        "sra_kernel_timing": [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -180,6 +182,24 @@ def schedule_export(samples, which: int, heads=1, head_dim=128):
 
 def release_caches() -> None:
     _check(lib().sra_release_caches())
+
+
+KERNELS = {"forward": 0, "delta": 1, "dkdv": 2, "dq": 3, "fill": 4}
+
+
+def kernel_timing_enable(on: bool = True) -> None:
+    """Brackets every kernel launch with hipEvents on its stream (and resets the totals)."""
+    _check(lib().sra_kernel_timing_enable(1 if on else 0))
+
+
+def kernel_timing() -> Dict[str, Tuple[float, int]]:
+    """{kernel: (total ms, launches)} since timing was enabled (waits for the events)."""
+    out = {}
+    for name, k in KERNELS.items():
+        ms, n = ctypes.c_double(0), ctypes.c_int64(0)
+        _check(lib().sra_kernel_timing(k, ctypes.byref(ms), ctypes.byref(n)))
+        out[name] = (float(ms.value), int(n.value))
+    return out
 
 
 # ----------------------------------------------------------------------------- device calls

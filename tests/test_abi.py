@@ -15,7 +15,8 @@ def test_library_exports_every_declared_function():
     names = sra.header_functions()
     assert set(names) >= {"sra_workspace_size", "sra_forward", "sra_backward", "sra_pair_counts",
                           "sra_schedule_info", "sra_schedule_mask", "sra_schedule_export",
-                          "sra_release_caches", "sra_status_string", "sra_last_error", "sra_version"}
+                          "sra_release_caches", "sra_status_string", "sra_last_error", "sra_version",
+                          "sra_kernel_timing_enable", "sra_kernel_timing"}
     L = sra.lib()
     for n in names:
         assert hasattr(L, n), n
