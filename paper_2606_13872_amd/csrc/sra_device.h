@@ -28,7 +28,7 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // Combine a value held by lanes l and l^32 (the two halves of one MFMA output column).
 __device__ __forceinline__ float pair_max(float x) {
   auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+  return __builtin_elementwise_maximum(__uint_as_float(s[0]), __uint_as_float(s[1]));
 }
 __device__ __forceinline__ float pair_sum(float x) {
   auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -44,6 +44,23 @@ __device__ __forceinline__ bf16x4 lds_read_tr(const __bf16* p) {
 __device__ __forceinline__ bf16x8 cat8(bf16x4 lo, bf16x4 hi) {
   return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
 }
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Sum of the 8 bf16 values of a fragment added to acc (fp32), two per V_DOT2C_F32_BF16.
+__device__ __forceinline__ float sum_bf16x8(bf16x8 v, float acc) {
+  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bf16x2 p = {v[2 * j], v[2 * j + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(p, one, acc, false);
+  }
+  return acc;
+}
+
+// IEEE-2019 maximum (V_MAXIMUM3_F32 on gfx950): needs no NaN canonicalisation of MFMA results.
+__device__ __forceinline__ float max2f(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float max3f(float a, float b, float c) { return max2f(a, max2f(b, c)); }
 
 // Eight consecutive accumulator registers -> bf16 (round to nearest even).
 __device__ __forceinline__ bf16x8 to_bf16x8(const floatx16& v, int base) {

@@ -1,18 +1,20 @@
 // Forward pass of Sparse Reference Attention on gfx950.
 //
-// One workgroup (4 wave64s) takes one work item: a tile of up to 256 query rows of one
-// stream and head, plus the list of key spans those rows see (Avatar V §1, §2.1, §4.3: gen
-// rows see the gen keys and the valid ref frames of their sample; ref rows see the valid
-// frames of their own group). Keys stream through LDS 64 rows at a time, double
-// buffered; every wave owns 64 query rows and keeps O^T in registers:
+// One workgroup (8 wave64s, two per SIMD) takes one work item: a tile of up to 256 query
+// rows of one stream and head, plus the list of key spans those rows see (Avatar V §1,
+// §2.1, §4.3: gen rows see the gen keys and the valid ref frames of their sample; ref rows
+// see the valid frames of their own group). Keys stream through LDS 64 rows at a time with
+// direct global->LDS loads into two buffers; every wave owns 32 query rows, and the two
+// waves of a SIMD overlap one's softmax (VALU) with the other's matrix products:
 //
 //   S^T (keys x queries) = K Q^T          bf16 MFMA 32x32x16, K rows from LDS, Q^T in VGPRs
 //   online softmax over keys in base 2, lanes = queries (row max/sum are lane-local plus
-//   one permlane32 swap); the running max is only moved when it grows by > 8 (log2), so
-//   the O rescale is rare
+//   one permlane32 swap); the running max only moves when it grows by more than 8 (log2),
+//   so rescaling O is rare
 //   O^T (d x queries) += V^T P^T          V^T fragments via the LDS transpose read
 //
-// Only the last step of a span is masked (its ragged tail); there is no dense mask.
+// Only the last step of a span (its ragged tail) runs the masked variant of the step;
+// there is no dense mask.
 #include "sra_kernels.h"
 #include "sra_tiles.h"
 
@@ -21,193 +23,191 @@ namespace sra {
 namespace {
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kRescaleSlack = 8.0f;  // log2 units: P may grow up to 2^8 before a rescale
+constexpr int kWaves = kFwdQueryTile / 32;
+template <int D> using KTile = PaddedTile<D, kFwdKeyStep, D + 8>;   // row-fragment reads
+template <int D> using VTile = PaddedTile<D, kFwdKeyStep, D + 16>;  // transpose reads
+}  // namespace
+
+template <int D>
+struct FwdState {
+  bf16x8 qf[D / 16];   // Q^T MFMA B fragments: lane = query, 8 consecutive head dims
+  floatx16 o[D / 32];  // O^T accumulators, 32 head dims each
+  float m;             // running max (log2 units)
+  float l;             // per-lane partial row sum (fp32)
+};
+
+// One 64-key step for the wave's 32 query rows. kMask: keys >= nvalid are outside the span.
+template <int D, bool kMask>
+__device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, const __bf16* vt, int nvalid,
+                                         float sl2) {
+  constexpr int NC = D / 16, ND = D / 32;
+  const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+  floatx16 s0 = floatx16{}, s1 = floatx16{};  // S^T for keys 0..31 and 32..63
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(kt + l32 * (D + 8) + c * 16 + half * 8);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(kt + (32 + l32) * (D + 8) + c * 16 + half * 8);
+    s0 = mfma32(k0, st.qf[c], s0);
+    s1 = mfma32(k1, st.qf[c], s1);
+  }
+  if constexpr (kMask) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int key = 8 * (i >> 2) + 4 * half + (i & 3);
+      s0[i] = key >= nvalid ? -INFINITY : s0[i];
+      s1[i] = key + 32 >= nvalid ? -INFINITY : s1[i];
+    }
+  }
+  float a = max2f(s0[0], s1[0]);
+#pragma unroll
+  for (int i = 1; i < 16; ++i) a = max3f(a, s0[i], s1[i]);
+  const float mx = pair_max(a) * sl2;
+  const bool grow = mx > st.m + kRescaleSlack;
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(grow) != 0, 0)) {
+    const float alpha = grow ? fast_exp2(st.m - mx) : 1.f;
+    st.m = grow ? mx : st.m;
+    st.l *= alpha;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) st.o[db] *= alpha;
+  }
+  const float nm = -st.m;
+  float acc = 0.f;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    s0[i] = fast_exp2(fmaf(s0[i], sl2, nm));
+    s1[i] = fast_exp2(fmaf(s1[i], sl2, nm));
+    acc += s0[i] + s1[i];
+  }
+  st.l += acc;
+  // O^T += V^T P^T: the transpose read gives lane (head dim l32) the 8 keys whose P values
+  // the B fragment holds, in the MFMA output's register order.
+  const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int trow = 4 * half + ((lane & 15) >> 2);
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2) {
+      const bf16x8 p = to_bf16x8(kb ? s1 : s0, 8 * c2);
+      const int r0 = kb * 32 + 16 * c2 + trow;
+#pragma unroll
+      for (int db = 0; db < ND; ++db) {
+        const bf16x8 va = cat8(lds_read_tr(vt + r0 * (D + 16) + db * 32 + tcol),
+                               lds_read_tr(vt + (r0 + 8) * (D + 16) + db * 32 + tcol));
+        st.o[db] = mfma32(va, p, st.o[db]);
+      }
+    }
 }
 
 template <int D>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_fwd_kernel(FwdArgs a) {
-  constexpr int NC = D / 16;  // 16-wide MFMA k-chunks over head_dim
-  constexpr int ND = D / 32;  // 32-row blocks of O^T
-  constexpr int BK = kFwdKeyStep;
-  __shared__ __attribute__((aligned(16))) __bf16 ks[2][BK * D];
-  __shared__ __attribute__((aligned(16))) __bf16 vs[2][BK * D];
+  constexpr int NC = D / 16, ND = D / 32, BK = kFwdKeyStep;
+  __shared__ __attribute__((aligned(1024))) __bf16 ks[2][KTile<D>::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 vs[2][VTile<D>::kElems];
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5, l32 = lane & 31;
   const int h = it.head, s = it.stream;
-  const int wrow0 = wave * 64;
+  const int wrow0 = wave * 32;
   const bool active = wrow0 < it.len;
   const float sl2 = a.scale_log2;
 
-  // Q^T as MFMA B fragments: lane holds query (l32) and 8 consecutive head dims.
-  bf16x8 qf[2][NC];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int r = wrow0 + qb * 32 + l32;
+  FwdState<D> st;
+  const int r = wrow0 + l32;
+  {
     const __bf16* src = a.q[s] + int64_t(it.start + min(r, it.len - 1)) * a.in_stride[s] + h * D + half * 8;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      bf16x8 x = *reinterpret_cast<const bf16x8*>(src + c * 16);
-      qf[qb][c] = (r < it.len) ? x : bf16x8{};
+      const bf16x8 x = *reinterpret_cast<const bf16x8*>(src + c * 16);
+      st.qf[c] = (r < it.len) ? x : bf16x8{};
     }
+#pragma unroll
+    for (int db = 0; db < ND; ++db) st.o[db] = floatx16{};
+    st.m = -INFINITY;
+    st.l = 0.f;
   }
-
-  floatx16 o[2][ND];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int db = 0; db < ND; ++db) o[qb][db] = floatx16{};
-  float m_run[2] = {-INFINITY, -INFINITY};
-  float l_part[2] = {0.f, 0.f};
 
   const Span* sp = a.spans + it.span_off;
   const int T = count_steps(sp, it.span_cnt, BK);
-  SpanCursor ld, cp;
+  SpanCursor ld;
   ld.init(sp, it.span_cnt);
-  cp.init(sp, it.span_cnt);
-  TileRegs<D, BK> kr, vr;
-
-  tile_load<D, BK>(kr, a.k[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-  tile_load<D, BK>(vr, a.v[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-  ld.advance(BK);
-  tile_store<D, BK>(kr, ks[0]);
-  tile_store<D, BK>(vr, vs[0]);
-  __syncthreads();
-  if (T > 1) {
-    tile_load<D, BK>(kr, a.k[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-    tile_load<D, BK>(vr, a.v[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-    ld.advance(BK);
+  TileLoader<D, BK, D + 8, kWaves> kl[2];
+  TileLoader<D, BK, D + 16, kWaves> vl[2];
+#pragma unroll
+  for (int ss = 0; ss < 2; ++ss) {
+    kl[ss].init(a.in_stride[ss], h, wave);
+    vl[ss].init(a.in_stride[ss], h, wave);
   }
+  auto issue = [&](int b) {
+    const int ss = ld.stream();
+    if (ld.off + BK <= ld.len()) {  // whole tile inside the span: fixed lane offsets
+      const int64_t row0 = int64_t(ld.start() + ld.off) * a.in_stride[ss];
+      if (ss == 0) {
+        kl[0].issue(ks[b], a.k[0] + row0, wave);
+        vl[0].issue(vs[b], a.v[0] + row0, wave);
+      } else {
+        kl[1].issue(ks[b], a.k[1] + row0, wave);
+        vl[1].issue(vs[b], a.v[1] + row0, wave);
+      }
+    } else {
+      tile_load_lds<D, BK, D + 8, kWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BK, D + 16, kWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+    }
+    ld.advance(BK);
+  };
 
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    const int nvalid = min(BK, cp.len() - cp.off);
-    if (active) {
-      const __bf16* kt = ks[buf];
-      const __bf16* vt = vs[buf];
-      floatx16 st[2][2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) st[kb][qb] = floatx16{};
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kt + tile_off<D>(kb * 32 + l32, c * 16 + half * 8));
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) st[kb][qb] = mfma32(ka, qf[qb][c], st[kb][qb]);
-        }
-      if (nvalid < BK) {  // ragged end of a span
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const int key = kb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
-            if (key >= nvalid) {
-              st[kb][0][i] = -INFINITY;
-              st[kb][1][i] = -INFINITY;
-            }
-          }
-      }
-      // online softmax, base 2, lazily rescaled
-      bool grow = false;
-      float alpha[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        float mx = st[0][qb][0];
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) mx = fmaxf(mx, st[kb][qb][i]);
-        mx = pair_max(mx) * sl2;
-        const bool need = mx > m_run[qb] + kRescaleSlack;
-        alpha[qb] = need ? fast_exp2(m_run[qb] - mx) : 1.f;
-        m_run[qb] = need ? mx : m_run[qb];
-        l_part[qb] *= alpha[qb];
-        grow |= need;
-      }
-      if (__builtin_amdgcn_ballot_w64(grow) != 0) {
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-          for (int db = 0; db < ND; ++db) o[qb][db] *= alpha[qb];
-      }
-      bf16x8 pf[2][2][2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            const float p = fast_exp2(fmaf(st[kb][qb][i], sl2, -m_run[qb]));
-            st[kb][qb][i] = p;
-            l_part[qb] += p;
-          }
-          pf[kb][qb][0] = to_bf16x8(st[kb][qb], 0);
-          pf[kb][qb][1] = to_bf16x8(st[kb][qb], 8);
-        }
-      // O^T += V^T P^T ; V^T fragment rows = keys matching the P^T register order
-      const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-      const int trow = 4 * half + ((lane & 15) >> 2);
-#pragma unroll
-      for (int db = 0; db < ND; ++db)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2) {
-            const int r0 = kb * 32 + 16 * c2 + trow;
-            const bf16x4 lo = lds_read_tr(vt + tile_off<D>(r0, db * 32 + tcol));
-            const bf16x4 hi = lds_read_tr(vt + tile_off<D>(r0 + 8, db * 32 + tcol));
-            const bf16x8 va = cat8(lo, hi);
-#pragma unroll
-            for (int qb = 0; qb < 2; ++qb) o[qb][db] = mfma32(va, pf[kb][qb][c2], o[qb][db]);
-          }
+  issue(0);
+  wait_vmem();
+  __syncthreads();
+  // Steps are numbered t over the whole span list (two LDS buffers alternate). Full steps of
+  // a span and its ragged last step run in separate loops, so the unmasked step carries no
+  // masking code at all.
+  int t = 0;
+  for (int si = 0; si < it.span_cnt; ++si) {
+    const int len = __builtin_amdgcn_readfirstlane(sp[si].len);
+    const int full = len / BK;
+    for (int j = 0; j < full; ++j, ++t) {
+      if (t + 1 < T) issue((t + 1) & 1);
+      if (active) fwd_step<D, false>(st, ks[t & 1], vs[t & 1], BK, sl2);
+      wait_vmem();
+      __syncthreads();
     }
-    cp.advance(BK);
-    if (t + 1 < T) {
-      tile_store<D, BK>(kr, ks[buf ^ 1]);
-      tile_store<D, BK>(vr, vs[buf ^ 1]);
-    }
-    __syncthreads();
-    if (t + 2 < T) {
-      tile_load<D, BK>(kr, a.k[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-      tile_load<D, BK>(vr, a.v[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-      ld.advance(BK);
+    if (len % BK) {
+      if (t + 1 < T) issue((t + 1) & 1);
+      if (active) fwd_step<D, true>(st, ks[t & 1], vs[t & 1], len % BK, sl2);
+      wait_vmem();
+      __syncthreads();
+      ++t;
     }
   }
 
   if (!active) return;
   const int64_t ostride = int64_t(a.heads) * D;
+  const float lt = pair_sum(st.l);
+  const float inv = 1.f / lt;
+  if (r < it.len) {
+    __bf16* orow = a.o[s] + int64_t(it.start + r) * ostride + h * D;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const float lt = pair_sum(l_part[qb]);
-    const float inv = 1.f / lt;
-    const int r = wrow0 + qb * 32 + l32;
-    if (r < it.len) {
-      __bf16* orow = a.o[s] + int64_t(it.start + r) * ostride + h * D;
+    for (int db = 0; db < ND; ++db)
 #pragma unroll
-      for (int db = 0; db < ND; ++db)
+      for (int g = 0; g < 4; ++g) {
+        bf16x4 w;
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          bf16x4 w;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) w[e] = (__bf16)(o[qb][db][4 * g + e] * inv);
-          *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * half) = w;
-        }
-      if (half == 0) a.lse[s][int64_t(h) * a.rows[s] + it.start + r] = (m_run[qb] + log2f(lt)) * kLn2;
-    }
+        for (int e = 0; e < 4; ++e) w[e] = (__bf16)(st.o[db][4 * g + e] * inv);
+        *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * half) = w;
+      }
+    if (half == 0) a.lse[s][int64_t(h) * a.rows[s] + it.start + r] = (st.m + log2f(lt)) * kLn2;
   }
 }
 
 hipError_t launch_forward(const FwdArgs& a, int n_items, int head_dim, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
   if (head_dim == 128)
-    hipLaunchKernelGGL(sra_fwd_kernel<128>, dim3(n_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(sra_fwd_kernel<128>, dim3(n_items), dim3(kWaves * 64), 0, stream, a);
   else
-    hipLaunchKernelGGL(sra_fwd_kernel<64>, dim3(n_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(sra_fwd_kernel<64>, dim3(n_items), dim3(kWaves * 64), 0, stream, a);
   return hipGetLastError();
 }
 

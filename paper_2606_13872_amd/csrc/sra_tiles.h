@@ -41,18 +41,110 @@ __device__ __forceinline__ void tile_store(const TileRegs<D, NR>& t, __bf16* lds
   }
 }
 
-// Walks the flattened sequence of NR-row steps over a work item's span list.
+// Padded LDS tiles: NR rows of D bf16, row stride RS elements (RS = D + 8 or D + 16). Every
+// fragment address is then one per-lane base plus a compile-time offset, and
+//  - RS = D + 8  (272 B rows for D = 128): 8 consecutive rows at one column fall in 8 distinct
+//    16-byte bank groups, so row fragments (ds_read_b128) are conflict-free;
+//  - RS = D + 16 (288 B rows): the 4 rows x 2 chunks of a transpose read fall in 8 distinct
+//    bank groups, so transpose reads are conflict-free.
+template <int D, int NR, int RS>
+struct PaddedTile {
+  static constexpr int kSlotsPerRow = RS / 8;                          // 16-byte slots per row
+  static constexpr int kInstr = (NR * kSlotsPerRow + 63) / 64;         // 1 KB load instructions
+  static constexpr int kElems = kInstr * 512;                          // LDS elements to reserve
+};
+
+// Direct global -> LDS copy (gfx950 GLOBAL_LOAD_LDS_DWORDX4) of rows [off, off + NR) of a span
+// into a padded tile. Each wave instruction fills 1 KB of LDS: lane l writes the 16 bytes at
+// (LDS base + 16 l), so lane l fetches the global chunk that belongs there; lanes that land on
+// a pad slot fetch an in-bounds chunk that nothing reads. Rows past the span end are clamped
+// to its last row (the kernels mask them). Instructions are dealt over the NW waves.
+template <int D, int NR, int RS, int NW>
+__device__ __forceinline__ void tile_load_lds(__bf16* lds, const __bf16* __restrict__ src, int64_t stride,
+                                              int head, int start, int len, int off, int wave) {
+  using TL = PaddedTile<D, NR, RS>;
+  constexpr int SPR = TL::kSlotsPerRow, CPR = D / 8;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int j = 0; j < (TL::kInstr + NW - 1) / NW; ++j) {
+    const int ins = wave + j * NW;
+    if (ins < TL::kInstr) {
+      const int p = ins * 64 + lane;
+      const int row = min(p / SPR, NR - 1);
+      const int slot = p % SPR;
+      const int ch = slot < CPR ? slot : 0;
+      const int rr = min(off + row, len - 1);
+      const __bf16* g = src + int64_t(start + rr) * stride + head * D + ch * 8;
+      __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(g),
+                                       (void __attribute__((address_space(3)))*)(lds + ins * 512), 16, 0, 0);
+    }
+  }
+}
+
+// Per-lane address offsets of the direct loads of a padded tile, for tiles whose NR rows all
+// lie inside the span (no clamping): lane offsets are fixed, only the tile's first row moves.
+template <int D, int NR, int RS, int NW>
+struct TileLoader {
+  using TL = PaddedTile<D, NR, RS>;
+  static constexpr int kSlots = (TL::kInstr + NW - 1) / NW;
+  int voff[kSlots];  // element offset of this lane's chunk from the tile's first row
+  __device__ __forceinline__ void init(int64_t stride, int head, int wave) {
+    constexpr int SPR = TL::kSlotsPerRow, CPR = D / 8;
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int j = 0; j < kSlots; ++j) {
+      const int p = (wave + j * NW) * 64 + lane;
+      const int row = min(p / SPR, NR - 1);
+      const int slot = p % SPR;
+      voff[j] = int(row * stride) + head * D + (slot < CPR ? slot : 0) * 8;
+    }
+  }
+  // `first_row` points at the tile's first row (uniform); every row is inside the span.
+  __device__ __forceinline__ void issue(__bf16* lds, const __bf16* first_row, int wave) const {
+#pragma unroll
+    for (int j = 0; j < kSlots; ++j) {
+      const int ins = wave + j * NW;
+      if (ins < TL::kInstr)
+        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(first_row + voff[j]),
+                                         (void __attribute__((address_space(3)))*)(lds + ins * 512), 16, 0, 0);
+    }
+  }
+};
+
+__device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Walks the flattened sequence of NR-row steps over a work item's span list, keeping the
+// current span's fields in registers (the span table is read once per span).
 struct SpanCursor {
   const Span* spans;
   int n, si, off;
-  __device__ __forceinline__ void init(const Span* s, int count) { spans = s; n = count; si = 0; off = 0; }
+  int cur_stream, cur_start, cur_len;
+  __device__ __forceinline__ void load() {
+    if (si < n) {
+      const Span s = spans[si];
+      cur_stream = __builtin_amdgcn_readfirstlane(s.stream);
+      cur_start = __builtin_amdgcn_readfirstlane(s.start);
+      cur_len = __builtin_amdgcn_readfirstlane(s.len);
+    }
+  }
+  __device__ __forceinline__ void init(const Span* s, int count) {
+    spans = s;
+    n = count;
+    si = 0;
+    off = 0;
+    load();
+  }
   __device__ __forceinline__ bool valid() const { return si < n; }
-  __device__ __forceinline__ int stream() const { return spans[si].stream; }
-  __device__ __forceinline__ int start() const { return spans[si].start; }
-  __device__ __forceinline__ int len() const { return spans[si].len; }
+  __device__ __forceinline__ int stream() const { return cur_stream; }
+  __device__ __forceinline__ int start() const { return cur_start; }
+  __device__ __forceinline__ int len() const { return cur_len; }
   __device__ __forceinline__ void advance(int step) {
     off += step;
-    if (off >= spans[si].len) { ++si; off = 0; }
+    if (off >= cur_len) {
+      ++si;
+      off = 0;
+      load();
+    }
   }
 };
 
