@@ -83,7 +83,7 @@ def test_schedule_tables_are_well_formed(which):
     samples = GEOMS[8]
     heads = 8
     items, spans = sra.schedule_export(samples, which, heads=heads)
-    tile = {sra.SCHED_FORWARD: 256, sra.SCHED_BWD_DQ: 256, sra.SCHED_BWD_DKDV: 128}[which]
+    tile = {sra.SCHED_FORWARD: 256, sra.SCHED_BWD_DQ: 256, sra.SCHED_BWD_DKDV: 256}[which]
     n_gen = sum(g.n_gen for g in samples)
     n_ref = sum(g.n_ref for g in samples)
     rows = (n_gen, n_ref)
