@@ -63,27 +63,73 @@ hipError_t launch_delta(const DeltaArgs& a, int head_dim, hipStream_t stream) {
 }
 
 // --------------------------------------------------------------------------- dq
+namespace {
+constexpr int kDqWaves = kDqQueryTile / 32;
+}
+
 template <int D>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+struct DqState {
+  bf16x8 qf[D / 16];    // Q^T B fragments (lane = query)
+  bf16x8 df[D / 16];    // dO^T B fragments (lane = query)
+  floatx16 dq[D / 32];  // dQ^T accumulators, 32 head dims each
+  float lse2, dlt;      // the row's log-sum-exp (log2 units) and rowsum(dO * O)
+};
+
+// One 32-key step of dQ for the wave's 32 query rows (S^T, dP^T with lanes = queries).
+template <int D, bool kMask>
+__device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const __bf16* vt, int nvalid,
+                                        float sl2) {
+  constexpr int NC = D / 16, ND = D / 32, RS = D + 8;
+  const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+  floatx16 s = floatx16{}, dp = floatx16{};
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kt + l32 * RS + c * 16 + half * 8);
+    const bf16x8 va = *reinterpret_cast<const bf16x8*>(vt + l32 * RS + c * 16 + half * 8);
+    s = mfma32(ka, st.qf[c], s);
+    dp = mfma32(va, st.df[c], dp);
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float p = fast_exp2(fmaf(s[i], sl2, -st.lse2));
+    if constexpr (kMask) p = (8 * (i >> 2) + 4 * half + (i & 3)) < nvalid ? p : 0.f;
+    s[i] = p * (dp[i] - st.dlt);
+  }
+  // dQ^T += K^T dS^T ; K^T fragments through the transpose read
+  const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int trow = 4 * half + ((lane & 15) >> 2);
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    const bf16x8 dsf = to_bf16x8(s, 8 * c2);
+    const int r0 = 16 * c2 + trow;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      const bf16x8 kta = cat8(lds_read_tr(kt + r0 * RS + db * 32 + tcol),
+                              lds_read_tr(kt + (r0 + 8) * RS + db * 32 + tcol));
+      st.dq[db] = mfma32(kta, dsf, st.dq[db]);
+    }
+  }
+}
+
+template <int D>
+__global__ void __launch_bounds__(kDqWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dq_kernel(BwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep;
-  __shared__ __attribute__((aligned(16))) __bf16 ks[2][BK * D];
-  __shared__ __attribute__((aligned(16))) __bf16 vs[2][BK * D];
+  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RS = D + 8;
+  using TL = PaddedTile<D, BK, RS>;
+  __shared__ __attribute__((aligned(1024))) __bf16 ks[2][TL::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 vs[2][TL::kElems];
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5, l32 = lane & 31;
   const int h = it.head, s = it.stream;
-  const int wrow0 = wave * 64;
-  const bool active = wrow0 < it.len;
+  const bool active = wave * 32 < it.len;
   const float sl2 = a.scale_log2;
 
-  bf16x8 qf[2][NC], df[2][NC];
-  float lse2[2], dlt[2];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int r = wrow0 + qb * 32 + l32;
+  DqState<D> st;
+  const int r = wave * 32 + l32;
+  {
     const int rr = it.start + min(r, it.len - 1);
     const __bf16* qs = a.q[s] + int64_t(rr) * a.in_stride[s] + h * D + half * 8;
     const __bf16* ds = a.dout[s] + int64_t(rr) * (int64_t(a.heads) * D) + h * D + half * 8;
@@ -91,275 +137,267 @@ sra_dq_kernel(BwdArgs a) {
     for (int c = 0; c < NC; ++c) {
       const bf16x8 x = *reinterpret_cast<const bf16x8*>(qs + c * 16);
       const bf16x8 y = *reinterpret_cast<const bf16x8*>(ds + c * 16);
-      qf[qb][c] = (r < it.len) ? x : bf16x8{};
-      df[qb][c] = (r < it.len) ? y : bf16x8{};
+      st.qf[c] = (r < it.len) ? x : bf16x8{};
+      st.df[c] = (r < it.len) ? y : bf16x8{};
     }
-    lse2[qb] = a.lse[s][int64_t(h) * a.rows[s] + rr] * kLog2e;
-    dlt[qb] = a.delta[s][int64_t(h) * a.rows[s] + rr];
+#pragma unroll
+    for (int db = 0; db < ND; ++db) st.dq[db] = floatx16{};
+    st.lse2 = a.lse[s][int64_t(h) * a.rows[s] + rr] * kLog2e;
+    st.dlt = a.delta[s][int64_t(h) * a.rows[s] + rr];
   }
-
-  floatx16 dq[2][ND];
-#pragma unroll
-  for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-    for (int db = 0; db < ND; ++db) dq[qb][db] = floatx16{};
 
   const Span* sp = a.spans + it.span_off;
   const int T = count_steps(sp, it.span_cnt, BK);
-  SpanCursor ld, cp;
+  SpanCursor ld;
   ld.init(sp, it.span_cnt);
-  cp.init(sp, it.span_cnt);
-  TileRegs<D, BK> kr, vr;
-  tile_load<D, BK>(kr, a.k[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-  tile_load<D, BK>(vr, a.v[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-  ld.advance(BK);
-  tile_store<D, BK>(kr, ks[0]);
-  tile_store<D, BK>(vr, vs[0]);
-  __syncthreads();
-  if (T > 1) {
-    tile_load<D, BK>(kr, a.k[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-    tile_load<D, BK>(vr, a.v[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
+  TileLoader<D, BK, RS, kDqWaves> kl[2], vl[2];
+#pragma unroll
+  for (int ss = 0; ss < 2; ++ss) {
+    kl[ss].init(a.in_stride[ss], h, wave);
+    vl[ss].init(a.in_stride[ss], h, wave);
+  }
+  auto issue = [&](int b) {
+    const int ss = ld.stream();
+    if (ld.off + BK <= ld.len()) {
+      const int64_t row0 = int64_t(ld.start() + ld.off) * a.in_stride[ss];
+      if (ss == 0) {
+        kl[0].issue(ks[b], a.k[0] + row0, wave);
+        vl[0].issue(vs[b], a.v[0] + row0, wave);
+      } else {
+        kl[1].issue(ks[b], a.k[1] + row0, wave);
+        vl[1].issue(vs[b], a.v[1] + row0, wave);
+      }
+    } else {
+      tile_load_lds<D, BK, RS, kDqWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BK, RS, kDqWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+    }
     ld.advance(BK);
-  }
-  const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int trow = 4 * half + ((lane & 15) >> 2);
+  };
 
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    const int nvalid = min(BK, cp.len() - cp.off);
-    if (active) {
-      const __bf16* kt = ks[buf];
-      const __bf16* vt = vs[buf];
-      floatx16 st[2], dpt[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        st[qb] = floatx16{};
-        dpt[qb] = floatx16{};
-      }
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kt + tile_off<D>(l32, c * 16 + half * 8));
-        const bf16x8 va = *reinterpret_cast<const bf16x8*>(vt + tile_off<D>(l32, c * 16 + half * 8));
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          st[qb] = mfma32(ka, qf[qb][c], st[qb]);
-          dpt[qb] = mfma32(va, df[qb][c], dpt[qb]);
-        }
-      }
-      bf16x8 dsf[2][2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = 8 * (i >> 2) + 4 * half + (i & 3);
-          float p = fast_exp2(fmaf(st[qb][i], sl2, -lse2[qb]));
-          p = key < nvalid ? p : 0.f;
-          st[qb][i] = p * (dpt[qb][i] - dlt[qb]);
-        }
-        dsf[qb][0] = to_bf16x8(st[qb], 0);
-        dsf[qb][1] = to_bf16x8(st[qb], 8);
-      }
-      // dQ^T += K^T dS^T ; K^T fragments through the transpose read
-#pragma unroll
-      for (int db = 0; db < ND; ++db)
-#pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2) {
-          const int r0 = 16 * c2 + trow;
-          const bf16x8 kta = cat8(lds_read_tr(kt + tile_off<D>(r0, db * 32 + tcol)),
-                                  lds_read_tr(kt + tile_off<D>(r0 + 8, db * 32 + tcol)));
-#pragma unroll
-          for (int qb = 0; qb < 2; ++qb) dq[qb][db] = mfma32(kta, dsf[qb][c2], dq[qb][db]);
-        }
+  issue(0);
+  wait_vmem();
+  __syncthreads();
+  int t = 0;
+  for (int si = 0; si < it.span_cnt; ++si) {
+    const int len = __builtin_amdgcn_readfirstlane(sp[si].len);
+    const int full = len / BK;
+    for (int j = 0; j < full; ++j, ++t) {
+      if (t + 1 < T) issue((t + 1) & 1);
+      if (active) dq_step<D, false>(st, ks[t & 1], vs[t & 1], BK, sl2);
+      wait_vmem();
+      __syncthreads();
     }
-    cp.advance(BK);
-    if (t + 1 < T) {
-      tile_store<D, BK>(kr, ks[buf ^ 1]);
-      tile_store<D, BK>(vr, vs[buf ^ 1]);
-    }
-    __syncthreads();
-    if (t + 2 < T) {
-      tile_load<D, BK>(kr, a.k[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-      tile_load<D, BK>(vr, a.v[ld.stream()], a.in_stride[ld.stream()], h, ld.start(), ld.len(), ld.off);
-      ld.advance(BK);
+    if (len % BK) {
+      if (t + 1 < T) issue((t + 1) & 1);
+      if (active) dq_step<D, true>(st, ks[t & 1], vs[t & 1], len % BK, sl2);
+      wait_vmem();
+      __syncthreads();
+      ++t;
     }
   }
 
-  if (!active) return;
-  const int64_t ostride = int64_t(a.heads) * D;
+  if (!active || r >= it.len) return;
+  __bf16* orow = a.dq[s] + int64_t(it.start + r) * (int64_t(a.heads) * D) + h * D;
 #pragma unroll
-  for (int qb = 0; qb < 2; ++qb) {
-    const int r = wrow0 + qb * 32 + l32;
-    if (r >= it.len) continue;
-    __bf16* orow = a.dq[s] + int64_t(it.start + r) * ostride + h * D;
+  for (int db = 0; db < ND; ++db)
 #pragma unroll
-    for (int db = 0; db < ND; ++db)
+    for (int g = 0; g < 4; ++g) {
+      bf16x4 w;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        bf16x4 w;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) w[e] = (__bf16)(dq[qb][db][4 * g + e] * a.scale);
-        *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * half) = w;
-      }
-  }
+      for (int e = 0; e < 4; ++e) w[e] = (__bf16)(st.dq[db][4 * g + e] * a.scale);
+      *reinterpret_cast<bf16x4*>(orow + db * 32 + 8 * g + 4 * half) = w;
+    }
 }
 
 hipError_t launch_dq(const BwdArgs& a, int n_items, int head_dim, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
   if (head_dim == 128)
-    hipLaunchKernelGGL(sra_dq_kernel<128>, dim3(n_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(sra_dq_kernel<128>, dim3(n_items), dim3(kDqWaves * 64), 0, stream, a);
   else
-    hipLaunchKernelGGL(sra_dq_kernel<64>, dim3(n_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(sra_dq_kernel<64>, dim3(n_items), dim3(kDqWaves * 64), 0, stream, a);
   return hipGetLastError();
 }
 
 // --------------------------------------------------------------------------- dkv
+namespace {
+constexpr int kDkvWaves = kDkvKeyTile / 32;
+}
+
 template <int D>
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+struct DkvState {
+  bf16x8 vf[D / 16];    // V as B fragments (lane = key, 8 consecutive head dims)
+  floatx16 dk[D / 32];  // dK^T accumulators (lane = key), 32 head dims each
+  floatx16 dv[D / 32];  // dV^T accumulators
+};
+
+// One 32-query step for the wave's 32 keys. S = Q K^T and dP = dO V^T have lanes = keys and
+// registers = query rows, so P and dS are directly the B fragments of dV^T += dO^T P and
+// dK^T += Q^T dS. kMask: query rows >= nvalid are outside the span.
+template <int D, bool kMask>
+__device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, const __bf16* qt,
+                                         const __bf16* dt, const float* lse_s, const float* dlt_s,
+                                         int nvalid, float sl2) {
+  constexpr int NC = D / 16, ND = D / 32, RQ = D + 16;
+  const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+  floatx16 s = floatx16{}, dp = floatx16{};
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qt + l32 * RQ + c * 16 + half * 8);
+    const bf16x8 kb = *reinterpret_cast<const bf16x8*>(krow + c * 16);
+    const bf16x8 da = *reinterpret_cast<const bf16x8*>(dt + l32 * RQ + c * 16 + half * 8);
+    s = mfma32(qa, kb, s);
+    dp = mfma32(da, st.vf[c], dp);
+  }
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const int q0 = 8 * g + 4 * half;  // 4 consecutive query rows of this register group
+    const floatx4 l4 = *reinterpret_cast<const floatx4*>(lse_s + q0);
+    const floatx4 d4 = *reinterpret_cast<const floatx4*>(dlt_s + q0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int i = 4 * g + e;
+      float p = fast_exp2(fmaf(s[i], sl2, -l4[e]));
+      if constexpr (kMask) p = (q0 + e) < nvalid ? p : 0.f;
+      s[i] = p;
+      dp[i] = p * (dp[i] - d4[e]);
+    }
+  }
+  // dV^T += dO^T P and dK^T += Q^T dS ; dO^T and Q^T fragments via the transpose read
+  const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  const int trow = 4 * half + ((lane & 15) >> 2);
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    const bf16x8 pb = to_bf16x8(s, 8 * c2);
+    const bf16x8 sb = to_bf16x8(dp, 8 * c2);
+    const int r0 = 16 * c2 + trow;
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      const bf16x8 dta = cat8(lds_read_tr(dt + r0 * RQ + db * 32 + tcol),
+                              lds_read_tr(dt + (r0 + 8) * RQ + db * 32 + tcol));
+      st.dv[db] = mfma32(dta, pb, st.dv[db]);
+      const bf16x8 qta = cat8(lds_read_tr(qt + r0 * RQ + db * 32 + tcol),
+                              lds_read_tr(qt + (r0 + 8) * RQ + db * 32 + tcol));
+      st.dk[db] = mfma32(qta, sb, st.dk[db]);
+    }
+  }
+}
+
+template <int D>
+__global__ void __launch_bounds__(kDkvWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dkv_kernel(BwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BQ = kDkvQueryStep;
-  __shared__ __attribute__((aligned(16))) __bf16 qs[2][BQ * D];
-  __shared__ __attribute__((aligned(16))) __bf16 dos[2][BQ * D];
+  constexpr int NC = D / 16, ND = D / 32, BQ = kDkvQueryStep, RK = D + 8, RQ = D + 16;
+  using KT = PaddedTile<D, kDkvKeyTile, RK>;
+  using QT = PaddedTile<D, BQ, RQ>;
+  __shared__ __attribute__((aligned(1024))) __bf16 ktile[KT::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 qs[2][QT::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 dos[2][QT::kElems];
   __shared__ __attribute__((aligned(16))) float lse_s[2][BQ];
   __shared__ __attribute__((aligned(16))) float dlt_s[2][BQ];
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int half = lane >> 5, l32 = lane & 31;
   const int h = it.head, s = it.stream;
-  const int wkey0 = wave * 32;
-  const bool active = wkey0 < it.len;
+  const bool active = wave * 32 < it.len;
   const float sl2 = a.scale_log2;
+  const int64_t dstride = int64_t(a.heads) * D;
 
-  // K and V as MFMA B fragments: lane holds key l32 and 8 consecutive head dims.
-  bf16x8 kf[NC], vf[NC];
+  // the item's keys: K rows into LDS (clamped at the tile end), V fragments into VGPRs
+  tile_load_lds<D, kDkvKeyTile, RK, kDkvWaves>(ktile, a.k[s], a.in_stride[s], h, it.start, it.len, 0, wave);
+  DkvState<D> st;
+  const int r = wave * 32 + l32;
   {
-    const int r = wkey0 + l32;
-    const int rr = it.start + min(r, it.len - 1);
-    const __bf16* kp = a.k[s] + int64_t(rr) * a.in_stride[s] + h * D + half * 8;
-    const __bf16* vp = a.v[s] + int64_t(rr) * a.in_stride[s] + h * D + half * 8;
+    const __bf16* vp = a.v[s] + int64_t(it.start + min(r, it.len - 1)) * a.in_stride[s] + h * D + half * 8;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
-      const bf16x8 x = *reinterpret_cast<const bf16x8*>(kp + c * 16);
       const bf16x8 y = *reinterpret_cast<const bf16x8*>(vp + c * 16);
-      kf[c] = (r < it.len) ? x : bf16x8{};
-      vf[c] = (r < it.len) ? y : bf16x8{};
+      st.vf[c] = (r < it.len) ? y : bf16x8{};
+    }
+#pragma unroll
+    for (int db = 0; db < ND; ++db) {
+      st.dk[db] = floatx16{};
+      st.dv[db] = floatx16{};
     }
   }
-  floatx16 dk[ND], dv[ND];
-#pragma unroll
-  for (int db = 0; db < ND; ++db) {
-    dk[db] = floatx16{};
-    dv[db] = floatx16{};
-  }
+  const __bf16* krow = ktile + r * RK + half * 8;
 
   const Span* sp = a.spans + it.span_off;
   const int T = count_steps(sp, it.span_cnt, BQ);
-  SpanCursor ld, cp;
+  SpanCursor ld;
   ld.init(sp, it.span_cnt);
-  cp.init(sp, it.span_cnt);
-  TileRegs<D, BQ> qr, dr;
-  float lr = 0.f, drr = 0.f;  // threads < BQ stage one row's LSE (log2 units) and delta
-
-  auto load_step = [&]() {
+  TileLoader<D, BQ, RQ, kDkvWaves> ql[2], dl;
+#pragma unroll
+  for (int ss = 0; ss < 2; ++ss) ql[ss].init(a.in_stride[ss], h, wave);
+  dl.init(dstride, h, wave);
+  float lr = 0.f, dr = 0.f;  // wave 0 lanes < BQ stage one row's LSE (log2 units) and delta
+  auto load_row_scalars = [&]() {
     const int ss = ld.stream();
-    tile_load<D, BQ>(qr, a.q[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off);
-    tile_load<D, BQ>(dr, a.dout[ss], int64_t(a.heads) * D, h, ld.start(), ld.len(), ld.off);
-    if (threadIdx.x < BQ) {
-      const int rr = ld.start() + min(ld.off + int(threadIdx.x), ld.len() - 1);
+    if (wave == 0 && lane < BQ) {
+      const int rr = ld.start() + min(ld.off + lane, ld.len() - 1);
       lr = a.lse[ss][int64_t(h) * a.rows[ss] + rr] * kLog2e;
-      drr = a.delta[ss][int64_t(h) * a.rows[ss] + rr];
+      dr = a.delta[ss][int64_t(h) * a.rows[ss] + rr];
     }
+  };
+  auto issue_tiles = [&](int b) {
+    const int ss = ld.stream();
+    if (ld.off + BQ <= ld.len()) {
+      const int64_t row0 = int64_t(ld.start() + ld.off);
+      if (ss == 0)
+        ql[0].issue(qs[b], a.q[0] + row0 * a.in_stride[0], wave);
+      else
+        ql[1].issue(qs[b], a.q[1] + row0 * a.in_stride[1], wave);
+      dl.issue(dos[b], a.dout[ss] + row0 * dstride, wave);
+    } else {
+      tile_load_lds<D, BQ, RQ, kDkvWaves>(qs[b], a.q[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BQ, RQ, kDkvWaves>(dos[b], a.dout[ss], dstride, h, ld.start(), ld.len(), ld.off, wave);
+    }
+    load_row_scalars();
     ld.advance(BQ);
   };
-  auto store_step = [&](int b) {
-    tile_store<D, BQ>(qr, qs[b]);
-    tile_store<D, BQ>(dr, dos[b]);
-    if (threadIdx.x < BQ) {
-      lse_s[b][threadIdx.x] = lr;
-      dlt_s[b][threadIdx.x] = drr;
+  auto stage_scalars = [&](int b) {
+    if (wave == 0 && lane < BQ) {
+      lse_s[b][lane] = lr;
+      dlt_s[b][lane] = dr;
     }
   };
 
-  load_step();
-  store_step(0);
+  issue_tiles(0);
+  stage_scalars(0);
+  wait_vmem();
   __syncthreads();
-  if (T > 1) load_step();
-  const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
-  const int trow = 4 * half + ((lane & 15) >> 2);
-
-  for (int t = 0; t < T; ++t) {
-    const int buf = t & 1;
-    const int nvalid = min(BQ, cp.len() - cp.off);
-    if (active) {
-      const __bf16* qt = qs[buf];
-      const __bf16* dt = dos[buf];
-      floatx16 st[2], dp[2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        st[qb] = floatx16{};
-        dp[qb] = floatx16{};
+  int t = 0;
+  for (int si = 0; si < it.span_cnt; ++si) {
+    const int len = __builtin_amdgcn_readfirstlane(sp[si].len);
+    const int full = len / BQ;
+    for (int j = 0; j < full; ++j, ++t) {
+      const int b = t & 1;
+      if (t + 1 < T) issue_tiles(b ^ 1);
+      if (active) dkv_step<D, false>(st, krow, qs[b], dos[b], lse_s[b], dlt_s[b], BQ, sl2);
+      if (t + 1 < T) {
+        wait_vmem();
+        stage_scalars(b ^ 1);
       }
-      // S = Q K^T and dP = dO V^T (rows = queries, lanes = keys)
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-          const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qt + tile_off<D>(qb * 32 + l32, c * 16 + half * 8));
-          const bf16x8 da = *reinterpret_cast<const bf16x8*>(dt + tile_off<D>(qb * 32 + l32, c * 16 + half * 8));
-          st[qb] = mfma32(qa, kf[c], st[qb]);
-          dp[qb] = mfma32(da, vf[c], dp[qb]);
-        }
-      bf16x8 pb[2][2], sb[2][2];
-#pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int q0 = qb * 32 + 8 * g + 4 * half;  // 4 consecutive query rows
-          const floatx4 l4 = *reinterpret_cast<const floatx4*>(&lse_s[buf][q0]);
-          const floatx4 d4 = *reinterpret_cast<const floatx4*>(&dlt_s[buf][q0]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int i = 4 * g + e;
-            float p = fast_exp2(fmaf(st[qb][i], sl2, -l4[e]));
-            p = (q0 + e) < nvalid ? p : 0.f;
-            st[qb][i] = p;
-            dp[qb][i] = p * (dp[qb][i] - d4[e]);
-          }
-        }
-        pb[qb][0] = to_bf16x8(st[qb], 0);
-        pb[qb][1] = to_bf16x8(st[qb], 8);
-        sb[qb][0] = to_bf16x8(dp[qb], 0);
-        sb[qb][1] = to_bf16x8(dp[qb], 8);
-      }
-      // dV^T += dO^T P and dK^T += Q^T dS ; dO^T and Q^T fragments via the transpose read
-#pragma unroll
-      for (int db = 0; db < ND; ++db)
-#pragma unroll
-        for (int qb = 0; qb < 2; ++qb)
-#pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2) {
-            const int r0 = qb * 32 + 16 * c2 + trow;
-            const bf16x8 dta = cat8(lds_read_tr(dt + tile_off<D>(r0, db * 32 + tcol)),
-                                    lds_read_tr(dt + tile_off<D>(r0 + 8, db * 32 + tcol)));
-            const bf16x8 qta = cat8(lds_read_tr(qt + tile_off<D>(r0, db * 32 + tcol)),
-                                    lds_read_tr(qt + tile_off<D>(r0 + 8, db * 32 + tcol)));
-            dv[db] = mfma32(dta, pb[qb][c2], dv[db]);
-            dk[db] = mfma32(qta, sb[qb][c2], dk[db]);
-          }
+      wait_vmem();
+      __syncthreads();
     }
-    cp.advance(BQ);
-    if (t + 1 < T) store_step(buf ^ 1);
-    __syncthreads();
-    if (t + 2 < T) load_step();
+    if (len % BQ) {
+      const int b = t & 1;
+      if (t + 1 < T) issue_tiles(b ^ 1);
+      if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], lse_s[b], dlt_s[b], len % BQ, sl2);
+      if (t + 1 < T) {
+        wait_vmem();
+        stage_scalars(b ^ 1);
+      }
+      wait_vmem();
+      __syncthreads();
+      ++t;
+    }
   }
 
-  if (!active) return;
-  const int r = wkey0 + l32;
-  if (r >= it.len) return;
-  const int64_t ostride = int64_t(a.heads) * D;
-  __bf16* krow = a.dk[s] + int64_t(it.start + r) * ostride + h * D;
-  __bf16* vrow = a.dv[s] + int64_t(it.start + r) * ostride + h * D;
+  if (!active || r >= it.len) return;
+  __bf16* kout = a.dk[s] + int64_t(it.start + r) * dstride + h * D;
+  __bf16* vout = a.dv[s] + int64_t(it.start + r) * dstride + h * D;
 #pragma unroll
   for (int db = 0; db < ND; ++db)
 #pragma unroll
@@ -367,20 +405,20 @@ sra_dkv_kernel(BwdArgs a) {
       bf16x4 wk, wv;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        wk[e] = (__bf16)(dk[db][4 * g + e] * a.scale);
-        wv[e] = (__bf16)(dv[db][4 * g + e]);
+        wk[e] = (__bf16)(st.dk[db][4 * g + e] * a.scale);
+        wv[e] = (__bf16)(st.dv[db][4 * g + e]);
       }
-      *reinterpret_cast<bf16x4*>(krow + db * 32 + 8 * g + 4 * half) = wk;
-      *reinterpret_cast<bf16x4*>(vrow + db * 32 + 8 * g + 4 * half) = wv;
+      *reinterpret_cast<bf16x4*>(kout + db * 32 + 8 * g + 4 * half) = wk;
+      *reinterpret_cast<bf16x4*>(vout + db * 32 + 8 * g + 4 * half) = wv;
     }
 }
 
 hipError_t launch_dkv(const BwdArgs& a, int n_items, int head_dim, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
   if (head_dim == 128)
-    hipLaunchKernelGGL(sra_dkv_kernel<128>, dim3(n_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(sra_dkv_kernel<128>, dim3(n_items), dim3(kDkvWaves * 64), 0, stream, a);
   else
-    hipLaunchKernelGGL(sra_dkv_kernel<64>, dim3(n_items), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL(sra_dkv_kernel<64>, dim3(n_items), dim3(kDkvWaves * 64), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -4,17 +4,17 @@
 
 namespace sra {
 
-// Forward: one workgroup = 4 wave64s, each wave owns 64 query rows (two 32-row MFMA
-// blocks), so a work item covers 256 query rows; keys stream through LDS 64 at a time.
+// Forward: one workgroup = 8 wave64s (two per SIMD), each wave owns 32 query rows, so a work
+// item covers 256 query rows; keys stream through LDS 64 at a time.
 constexpr int kFwdQueryTile = 256;
 constexpr int kFwdKeyStep = 64;
-// dQ kernel of the backward: same query tiling, 32-key steps (3 products per step).
+// dQ kernel of the backward: same query tiling (8 waves x 32 rows), 32-key steps.
 constexpr int kDqQueryTile = 256;
 constexpr int kDqKeyStep = 32;
-// dK/dV kernel of the backward: 4 waves x 32 keys = 128 keys per work item; queries stream
-// through LDS 64 at a time.
-constexpr int kDkvKeyTile = 128;
-constexpr int kDkvQueryStep = 64;
+// dK/dV kernel of the backward: 8 waves x 32 keys = 256 keys per work item; queries stream
+// through LDS 32 at a time.
+constexpr int kDkvKeyTile = 256;
+constexpr int kDkvQueryStep = 32;
 
 constexpr int kThreads = 256;
 constexpr int kNumXcd = 8;  // MI355X: 8 accelerator complex dies; workgroups go round-robin
