@@ -79,13 +79,13 @@ struct DqState {
 template <int D, bool kMask>
 __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const __bf16* vt, int nvalid,
                                         float sl2) {
-  constexpr int NC = D / 16, ND = D / 32, RS = D + 8;
+  constexpr int NC = D / 16, ND = D / 32, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
   floatx16 s = floatx16{}, dp = floatx16{};
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kt + l32 * RS + c * 16 + half * 8);
-    const bf16x8 va = *reinterpret_cast<const bf16x8*>(vt + l32 * RS + c * 16 + half * 8);
+    const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kt + l32 * RK + c * 16 + half * 8);
+    const bf16x8 va = *reinterpret_cast<const bf16x8*>(vt + l32 * RV + c * 16 + half * 8);
     s = mfma32(ka, st.qf[c], s);
     dp = mfma32(va, st.df[c], dp);
   }
@@ -104,8 +104,8 @@ __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const 
     const int r0 = 16 * c2 + trow;
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
-      const bf16x8 kta = cat8(lds_read_tr(kt + r0 * RS + db * 32 + tcol),
-                              lds_read_tr(kt + (r0 + 8) * RS + db * 32 + tcol));
+      const bf16x8 kta = cat8(lds_read_tr(kt + r0 * RK + db * 32 + tcol),
+                              lds_read_tr(kt + (r0 + 8) * RK + db * 32 + tcol));
       st.dq[db] = mfma32(kta, dsf, st.dq[db]);
     }
   }
@@ -114,10 +114,9 @@ __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const 
 template <int D>
 __global__ void __launch_bounds__(kDqWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dq_kernel(BwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RS = D + 8;
-  using TL = PaddedTile<D, BK, RS>;
-  __shared__ __attribute__((aligned(1024))) __bf16 ks[2][TL::kElems];
-  __shared__ __attribute__((aligned(1024))) __bf16 vs[2][TL::kElems];
+  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
+  __shared__ __attribute__((aligned(1024))) __bf16 ks[2][PaddedTile<D, BK, RK>::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 vs[2][PaddedTile<D, BK, RV>::kElems];
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
@@ -150,7 +149,8 @@ sra_dq_kernel(BwdArgs a) {
   const int T = count_steps(sp, it.span_cnt, BK);
   SpanCursor ld;
   ld.init(sp, it.span_cnt);
-  TileLoader<D, BK, RS, kDqWaves> kl[2], vl[2];
+  TileLoader<D, BK, RK, kDqWaves> kl[2];
+  TileLoader<D, BK, RV, kDqWaves> vl[2];
 #pragma unroll
   for (int ss = 0; ss < 2; ++ss) {
     kl[ss].init(a.in_stride[ss], h, wave);
@@ -168,8 +168,8 @@ sra_dq_kernel(BwdArgs a) {
         vl[1].issue(vs[b], a.v[1] + row0, wave);
       }
     } else {
-      tile_load_lds<D, BK, RS, kDqWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
-      tile_load_lds<D, BK, RS, kDqWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BK, RK, kDqWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BK, RV, kDqWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
     }
     ld.advance(BK);
   };
@@ -237,7 +237,7 @@ template <int D, bool kMask>
 __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, const __bf16* qt,
                                          const __bf16* dt, const float* lse_s, const float* dlt_s,
                                          int nvalid, float sl2) {
-  constexpr int NC = D / 16, ND = D / 32, RQ = D + 16;
+  constexpr int NC = D / 16, ND = D / 32, RQ = kBothPadRS<D>;
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
   floatx16 s = floatx16{}, dp = floatx16{};
 #pragma unroll
@@ -285,7 +285,7 @@ __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, co
 template <int D>
 __global__ void __launch_bounds__(kDkvWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dkv_kernel(BwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BQ = kDkvQueryStep, RK = D + 8, RQ = D + 16;
+  constexpr int NC = D / 16, ND = D / 32, BQ = kDkvQueryStep, RK = kRowPadRS<D>, RQ = kBothPadRS<D>;
   using KT = PaddedTile<D, kDkvKeyTile, RK>;
   using QT = PaddedTile<D, BQ, RQ>;
   __shared__ __attribute__((aligned(1024))) __bf16 ktile[KT::kElems];

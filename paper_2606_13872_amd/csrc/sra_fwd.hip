@@ -24,8 +24,8 @@ namespace {
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kRescaleSlack = 8.0f;  // log2 units: P may grow up to 2^8 before a rescale
 constexpr int kWaves = kFwdQueryTile / 32;
-template <int D> using KTile = PaddedTile<D, kFwdKeyStep, D + 8>;   // row-fragment reads
-template <int D> using VTile = PaddedTile<D, kFwdKeyStep, D + 16>;  // transpose reads
+template <int D> using KTile = PaddedTile<D, kFwdKeyStep, kRowPadRS<D>>;  // row-fragment reads
+template <int D> using VTile = PaddedTile<D, kFwdKeyStep, kTrPadRS<D>>;   // transpose reads
 }  // namespace
 
 template <int D>
@@ -45,8 +45,8 @@ __device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, cons
   floatx16 s0 = floatx16{}, s1 = floatx16{};  // S^T for keys 0..31 and 32..63
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(kt + l32 * (D + 8) + c * 16 + half * 8);
-    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(kt + (32 + l32) * (D + 8) + c * 16 + half * 8);
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(kt + l32 * kRowPadRS<D> + c * 16 + half * 8);
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(kt + (32 + l32) * kRowPadRS<D> + c * 16 + half * 8);
     s0 = mfma32(k0, st.qf[c], s0);
     s1 = mfma32(k1, st.qf[c], s1);
   }
@@ -58,9 +58,15 @@ __device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, cons
       s1[i] = key + 32 >= nvalid ? -INFINITY : s1[i];
     }
   }
-  float a = max2f(s0[0], s1[0]);
+  // row max as a 4-way tree (short dependency chains)
+  float mq[4];
 #pragma unroll
-  for (int i = 1; i < 16; ++i) a = max3f(a, s0[i], s1[i]);
+  for (int j = 0; j < 4; ++j) mq[j] = max3f(max2f(s0[4 * j], s1[4 * j]), s0[4 * j + 1], s1[4 * j + 1]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) mq[j] = max3f(mq[j], s0[4 * j + 2], s1[4 * j + 2]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) mq[j] = max3f(mq[j], s0[4 * j + 3], s1[4 * j + 3]);
+  const float a = max2f(max2f(mq[0], mq[1]), max2f(mq[2], mq[3]));
   const float mx = pair_max(a) * sl2;
   const bool grow = mx > st.m + kRescaleSlack;
   if (__builtin_expect(__builtin_amdgcn_ballot_w64(grow) != 0, 0)) {
@@ -71,14 +77,14 @@ __device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, cons
     for (int db = 0; db < ND; ++db) st.o[db] *= alpha;
   }
   const float nm = -st.m;
-  float acc = 0.f;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};  // 4 independent partial sums
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     s0[i] = fast_exp2(fmaf(s0[i], sl2, nm));
     s1[i] = fast_exp2(fmaf(s1[i], sl2, nm));
-    acc += s0[i] + s1[i];
+    acc[i & 3] += s0[i] + s1[i];
   }
-  st.l += acc;
+  st.l += (acc[0] + acc[1]) + (acc[2] + acc[3]);
   // O^T += V^T P^T: the transpose read gives lane (head dim l32) the 8 keys whose P values
   // the B fragment holds, in the MFMA output's register order.
   const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -91,8 +97,8 @@ __device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, cons
       const int r0 = kb * 32 + 16 * c2 + trow;
 #pragma unroll
       for (int db = 0; db < ND; ++db) {
-        const bf16x8 va = cat8(lds_read_tr(vt + r0 * (D + 16) + db * 32 + tcol),
-                               lds_read_tr(vt + (r0 + 8) * (D + 16) + db * 32 + tcol));
+        const bf16x8 va = cat8(lds_read_tr(vt + r0 * kTrPadRS<D> + db * 32 + tcol),
+                               lds_read_tr(vt + (r0 + 8) * kTrPadRS<D> + db * 32 + tcol));
         st.o[db] = mfma32(va, p, st.o[db]);
       }
     }
@@ -133,8 +139,8 @@ sra_fwd_kernel(FwdArgs a) {
   const int T = count_steps(sp, it.span_cnt, BK);
   SpanCursor ld;
   ld.init(sp, it.span_cnt);
-  TileLoader<D, BK, D + 8, kWaves> kl[2];
-  TileLoader<D, BK, D + 16, kWaves> vl[2];
+  TileLoader<D, BK, kRowPadRS<D>, kWaves> kl[2];
+  TileLoader<D, BK, kTrPadRS<D>, kWaves> vl[2];
 #pragma unroll
   for (int ss = 0; ss < 2; ++ss) {
     kl[ss].init(a.in_stride[ss], h, wave);
@@ -152,8 +158,8 @@ sra_fwd_kernel(FwdArgs a) {
         vl[1].issue(vs[b], a.v[1] + row0, wave);
       }
     } else {
-      tile_load_lds<D, BK, D + 8, kWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
-      tile_load_lds<D, BK, D + 16, kWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BK, kRowPadRS<D>, kWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BK, kTrPadRS<D>, kWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
     }
     ld.advance(BK);
   };

@@ -41,12 +41,20 @@ __device__ __forceinline__ void tile_store(const TileRegs<D, NR>& t, __bf16* lds
   }
 }
 
-// Padded LDS tiles: NR rows of D bf16, row stride RS elements (RS = D + 8 or D + 16). Every
-// fragment address is then one per-lane base plus a compile-time offset, and
-//  - RS = D + 8  (272 B rows for D = 128): 8 consecutive rows at one column fall in 8 distinct
-//    16-byte bank groups, so row fragments (ds_read_b128) are conflict-free;
-//  - RS = D + 16 (288 B rows): the 4 rows x 2 chunks of a transpose read fall in 8 distinct
-//    bank groups, so transpose reads are conflict-free.
+// Padded LDS tiles: NR rows of D bf16 with a row stride of RS elements, so every fragment
+// address is one per-lane base plus a compile-time offset. The stride decides the bank
+// pattern; measured on gfx950 (LDS read bytes per clock per CU, 16-byte aligned strides):
+//   row stride (D = 128)   row fragment (ds_read_b128)   transpose read (ds_read_b64_tr_b16)
+//   256 B                   16                            64
+//   272 B  (D + 8)         128                            64
+//   288 B  (D + 16)         64                           122
+//   304 B  (D + 24)        128                           122
+//   320 B  (D + 32)         32                           203
+// so tiles read only as row fragments use D + 8, tiles read only through the transpose read
+// use D + 32, and tiles read both ways use D + 24.
+template <int D> constexpr int kRowPadRS = D + 8;
+template <int D> constexpr int kTrPadRS = D + 32;
+template <int D> constexpr int kBothPadRS = D + 24;
 template <int D, int NR, int RS>
 struct PaddedTile {
   static constexpr int kSlotsPerRow = RS / 8;                          // 16-byte slots per row
