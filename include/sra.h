@@ -7,7 +7,7 @@
  *     reference (ref) key of its sample, through ONE softmax over the concatenated key set
  *     (§4.3 concatenates the cached reference K/V with the generation K/V);
  *   - every ref query attends only to the ref keys of its own self-attention group, never to
- *     gen keys (§1, §8: reference tokens only self-attend). A group is `group_frames`
+ *     gen keys (§1, §8.2: the reference side attends only within itself). A group is `group_frames`
  *     consecutive reference latent frames; group_frames = 1 keeps the cost linear in the
  *     reference length (§1, §2.1);
  *   - tokens of invalid reference frames (§4.3, e.g. frames where the face is not visible)

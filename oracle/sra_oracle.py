@@ -10,8 +10,8 @@ What it computes (Avatar V, §1 contributions; §2.1 "Sparse Reference Attention
   * Generation (gen) queries attend to every generation key and to every valid
     reference (ref) key, through ONE softmax over the concatenation of the two key sets
     (§4.3: the cached reference K/V are concatenated with the generation K/V).
-  * Reference queries attend only to reference keys ("reference tokens only
-    self-attend", §1 and §8). The group a reference query sees is its own latent frame
+  * Reference queries attend only to reference keys, never to generation keys
+    (§1 and §8.2 state that the reference side attends only within itself). The group a reference query sees is its own latent frame
     by default (group_frames = 1); see the module note below.
   * Invalid reference frames (§4.3: e.g. frames where the face is not visible) are
     removed as keys for every query and as queries (output 0, log-sum-exp -inf,
@@ -24,8 +24,8 @@ backward pass is the textbook gradient of that masked softmax attention. Everyth
 computed in float64 by default (float32 on request), with numpy matmul as the only
 library primitive.
 
-Reading of the paper taken here (it gives no formula): "reference tokens only
-self-attend" combined with the claim of cost linear in reference length means a
+Reading of the paper taken here (it gives no formula): reference-only attention for
+reference queries, combined with the claim of cost linear in reference length means a
 reference query cannot see all reference keys (that would be quadratic in reference
 length); the smallest grouping consistent with both is one latent frame, which is the
 default. Larger groups (up to the whole reference clip) are a parameter.
@@ -64,8 +64,8 @@ def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
 
     M[q, k] is True when query q may attend to key k:
       gen q, gen k : True                               (full base self-attention)
-      gen q, ref k : valid(frame(k))                    (§1: gen attends to all reference tokens)
-      ref q, gen k : False                              (§1, §8: reference only self-attends)
+      gen q, ref k : valid(frame(k))                    (§1: gen sees every reference token)
+      ref q, gen k : False                              (§1, §8.2: reference attends only within itself)
       ref q, ref k : valid(frame(q)) and valid(frame(k)) and group(q) == group(k)
     `rows` selects a subset of query rows (row-block mode for large shapes).
     """
