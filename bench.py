@@ -15,6 +15,8 @@ length at the 480p sweep shape, and the CPU oracle on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
 import sys
@@ -26,6 +28,14 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0
 METRIC = "SRA useful TFLOP/s + % bf16 MFMA peak; ms/layer vs reference length"
+CSRC = os.path.join(ROOT, "paper_2606_13872_amd", "csrc")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_720p.json")
+KERNEL_SYMBOLS = {"forward": "sra_fwd_kernel", "dkdv": "sra_dkv_kernel", "dq": "sra_dq_kernel",
+                  "delta": "sra_delta_kernel"}
+KERNEL_SOURCES = {"forward": ["sra_fwd.hip"], "dkdv": ["sra_bwd.hip"], "dq": ["sra_bwd.hip"],
+                  "delta": ["sra_bwd.hip"]}
+COMMON_SOURCES = ["sra_config.h", "sra_device.h", "sra_tiles.h", "sra_kernels.h"]
+COPY_KERNEL = "neg_kernel"  # calibration: torch.neg over a float32 buffer reads and writes it once
 
 
 def _args():
@@ -36,7 +46,80 @@ def _args():
     ap.add_argument("--workload", default="720p", help="720p (default) or varlen")
     ap.add_argument("--sweep-reps", type=int, default=2, help="forward calls per sweep point (0 = skip)")
     ap.add_argument("--cpu-rows", type=int, default=3072, help="gen rows in the CPU-oracle sample (0 = skip)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="run one plain copy kernel (torch.neg, fp32) over this many MiB first: the "
+                         "calibration for the HBM byte counters")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="no GPU: turn two rocprofv3 --pmc counter files (FETCH_SIZE, WRITE_SIZE) of a "
+                         "--copy-mib run into per-launch HBM bytes per kernel, written to --traffic-out")
+    ap.add_argument("--traffic-out", default=TRAFFIC_FILE)
     return ap.parse_args()
+
+
+def _kernel_source_hash(kernel):
+    """Hash of the sources a kernel is built from: stored traffic is only used while it matches."""
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel] + COMMON_SOURCES:
+        h.update(f.encode())
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _counter_per_dispatch(path, counter):
+    """{short kernel name: (mean counter value per dispatch, dispatches)} from a rocprofv3 csv."""
+    tot, disp = {}, {}
+    with open(path, newline="") as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = next((k for k, sym in KERNEL_SYMBOLS.items() if sym in name), None)
+            if key is None and COPY_KERNEL in name:
+                key = "copy"
+            if key is None:
+                continue
+            tot[key] = tot.get(key, 0.0) + float(r["Counter_Value"])
+            disp.setdefault(key, set()).add(r["Dispatch_Id"])
+    return {k: (tot[k] / len(disp[k]), len(disp[k])) for k in tot}
+
+
+def _pmc_summary(fetch_csv, write_csv, copy_mib, workload_name, out_path):
+    """Per-launch HBM bytes of each kernel: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
+    scaled so that the copy kernel of known size reads and writes exactly its buffer."""
+    fetch = _counter_per_dispatch(fetch_csv, "FETCH_SIZE")
+    write = _counter_per_dispatch(write_csv, "WRITE_SIZE")
+    if "copy" not in fetch or "copy" not in write:
+        raise SystemExit("the counter files hold no copy-kernel dispatch: profile a --copy-mib run")
+    known_kib = copy_mib * 1024.0
+    fs, ws = known_kib / fetch["copy"][0], known_kib / write["copy"][0]
+    kernels = {}
+    for k in KERNEL_SYMBOLS:
+        if k in fetch and k in write:
+            kernels[k] = {"symbol": KERNEL_SYMBOLS[k], "source_hash": _kernel_source_hash(k),
+                          "fetch_bytes": round(fetch[k][0] * fs * 1024), "write_bytes": round(write[k][0] * ws * 1024),
+                          "fetch_kib_raw": fetch[k][0], "write_kib_raw": write[k][0], "dispatches": fetch[k][1]}
+    data = {"workload": workload_name,
+            "calibration": {"kernel": f"{COPY_KERNEL} over {copy_mib} MiB of float32",
+                            "fetch_kib_raw": fetch["copy"][0], "write_kib_raw": write["copy"][0],
+                            "fetch_scale": fs, "write_scale": ws},
+            "kernels": kernels}
+    with open(out_path, "w") as fh:
+        json.dump(data, fh, indent=1)
+    print(json.dumps(data, indent=1))
+
+
+def _stored_traffic(kernel, workload_name):
+    """HBM bytes per launch of `kernel` from the counter runs, or None if absent or stale."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            data = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    k = data.get("kernels", {}).get(kernel)
+    if data.get("workload") != workload_name or not k or k.get("source_hash") != _kernel_source_hash(kernel):
+        return None
+    return int(k["fetch_bytes"]) + int(k["write_bytes"])
 
 
 def _workload_config(w):
@@ -139,9 +222,12 @@ def _cpu_baseline(x_gpu, w, gen_rows, torch):
 
 def main():
     args = _args()
+    if args.pmc_summary:
+        _pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.copy_mib, args.workload, args.traffic_out)
+        return
     if args.gpus != 1:
-        print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are not part of "
-                                   "this build (heads shard across GPUs without collectives in the kernel)"}))
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; the library has no multi-GPU "
+                                   "path (heads would shard across GPUs with no collective inside the kernels)"}))
         sys.exit(2)
     import torch
 
@@ -167,6 +253,13 @@ def main():
     p = sra.Problem(w.samples, H, d)
     fo["workspace"] = torch.empty(p.workspace_size(False), dtype=torch.uint8, device=dev)
     bo["workspace"] = torch.empty(p.workspace_size(True), dtype=torch.uint8, device=dev)
+
+    if args.copy_mib > 0:
+        src = torch.ones(args.copy_mib * 262144, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         sra.forward(*ins, w.samples, out=fo)
@@ -201,7 +294,8 @@ def main():
     achieved = kernel_flops[dom] / (avg[dom] * 1e-3) / 1e12
     roofline = {"kernel": {"forward": "sra_fwd_kernel", "dkdv": "sra_dkv_kernel", "dq": "sra_dq_kernel"}[dom],
                 "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": _stored_traffic(dom, w.name),
+                "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                 "avg_launch_ms": round(avg[dom], 3),
                 "per_kernel_ms": {k: round(avg[k], 3) for k in avg if kt[k][1]}}
     line = {
