@@ -77,9 +77,9 @@ struct DqState {
 
 // One 32-key step of dQ for the wave's 32 query rows (S^T, dP^T with lanes = queries).
 template <int D, bool kMask>
-__device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const __bf16* vt, int nvalid,
-                                        float sl2) {
-  constexpr int NC = D / 16, ND = D / 32, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
+__device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const __bf16* ktt, const __bf16* vt,
+                                        int nvalid, float sl2) {
+  constexpr int NC = D / 16, ND = D / 32, RK = kRowPadRS<D>, RKT = kTrPadRS<D>, RV = kRowPadRS<D>;
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
   floatx16 s = floatx16{}, dp = floatx16{};
 #pragma unroll
@@ -104,8 +104,8 @@ __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const 
     const int r0 = 16 * c2 + trow;
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
-      const bf16x8 kta = cat8(lds_read_tr(kt + r0 * RK + db * 32 + tcol),
-                              lds_read_tr(kt + (r0 + 8) * RK + db * 32 + tcol));
+      const bf16x8 kta = cat8(lds_read_tr(ktt + r0 * RKT + db * 32 + tcol),
+                              lds_read_tr(ktt + (r0 + 8) * RKT + db * 32 + tcol));
       st.dq[db] = mfma32(kta, dsf, st.dq[db]);
     }
   }
@@ -114,8 +114,11 @@ __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const 
 template <int D>
 __global__ void __launch_bounds__(kDqWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dq_kernel(BwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
+  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RK = kRowPadRS<D>, RKT = kTrPadRS<D>,
+                RV = kRowPadRS<D>;
+  // K is staged twice: at the row-fragment stride and at the transpose-read stride
   __shared__ __attribute__((aligned(1024))) __bf16 ks[2][PaddedTile<D, BK, RK>::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 kts[2][PaddedTile<D, BK, RKT>::kElems];
   __shared__ __attribute__((aligned(1024))) __bf16 vs[2][PaddedTile<D, BK, RV>::kElems];
 
   const WorkItem it = a.items[blockIdx.x];
@@ -150,10 +153,12 @@ sra_dq_kernel(BwdArgs a) {
   SpanCursor ld;
   ld.init(sp, it.span_cnt);
   TileLoader<D, BK, RK, kDqWaves> kl[2];
+  TileLoader<D, BK, RKT, kDqWaves> ktl[2];
   TileLoader<D, BK, RV, kDqWaves> vl[2];
 #pragma unroll
   for (int ss = 0; ss < 2; ++ss) {
     kl[ss].init(a.in_stride[ss], h, wave);
+    ktl[ss].init(a.in_stride[ss], h, wave);
     vl[ss].init(a.in_stride[ss], h, wave);
   }
   auto issue = [&](int b) {
@@ -162,13 +167,16 @@ sra_dq_kernel(BwdArgs a) {
       const int64_t row0 = int64_t(ld.start() + ld.off) * a.in_stride[ss];
       if (ss == 0) {
         kl[0].issue(ks[b], a.k[0] + row0, wave);
+        ktl[0].issue(kts[b], a.k[0] + row0, wave);
         vl[0].issue(vs[b], a.v[0] + row0, wave);
       } else {
         kl[1].issue(ks[b], a.k[1] + row0, wave);
+        ktl[1].issue(kts[b], a.k[1] + row0, wave);
         vl[1].issue(vs[b], a.v[1] + row0, wave);
       }
     } else {
       tile_load_lds<D, BK, RK, kDqWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BK, RKT, kDqWaves>(kts[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
       tile_load_lds<D, BK, RV, kDqWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
     }
     ld.advance(BK);
@@ -183,13 +191,13 @@ sra_dq_kernel(BwdArgs a) {
     const int full = len / BK;
     for (int j = 0; j < full; ++j, ++t) {
       if (t + 1 < T) issue((t + 1) & 1);
-      if (active) dq_step<D, false>(st, ks[t & 1], vs[t & 1], BK, sl2);
+      if (active) dq_step<D, false>(st, ks[t & 1], kts[t & 1], vs[t & 1], BK, sl2);
       wait_vmem();
       __syncthreads();
     }
     if (len % BK) {
       if (t + 1 < T) issue((t + 1) & 1);
-      if (active) dq_step<D, true>(st, ks[t & 1], vs[t & 1], len % BK, sl2);
+      if (active) dq_step<D, true>(st, ks[t & 1], kts[t & 1], vs[t & 1], len % BK, sl2);
       wait_vmem();
       __syncthreads();
       ++t;
@@ -282,17 +290,26 @@ __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, co
   }
 }
 
-template <int D>
+// Query tiles rotate through kDkvBufs LDS buffers and the workgroup meets at a barrier only
+// after every second step, so the two waves of a SIMD can drift apart by up to a step and
+// overlap one's softmax with the other's matrix products. Tiles are loaded two steps ahead.
+// kOneStride: gen and ref q share one token stride, so one set of loader offsets serves both.
+namespace {
+constexpr int kDkvBufs = 4;
+}
+
+template <int D, bool kOneStride>
 __global__ void __launch_bounds__(kDkvWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dkv_kernel(BwdArgs a) {
   constexpr int NC = D / 16, ND = D / 32, BQ = kDkvQueryStep, RK = kRowPadRS<D>, RQ = kBothPadRS<D>;
+  constexpr int NB = kDkvBufs;
   using KT = PaddedTile<D, kDkvKeyTile, RK>;
   using QT = PaddedTile<D, BQ, RQ>;
   __shared__ __attribute__((aligned(1024))) __bf16 ktile[KT::kElems];
-  __shared__ __attribute__((aligned(1024))) __bf16 qs[2][QT::kElems];
-  __shared__ __attribute__((aligned(1024))) __bf16 dos[2][QT::kElems];
-  __shared__ __attribute__((aligned(16))) float lse_s[2][BQ];
-  __shared__ __attribute__((aligned(16))) float dlt_s[2][BQ];
+  __shared__ __attribute__((aligned(1024))) __bf16 qs[NB][QT::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 dos[NB][QT::kElems];
+  __shared__ __attribute__((aligned(16))) float lse_s[NB][BQ];
+  __shared__ __attribute__((aligned(16))) float dlt_s[NB][BQ];
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
@@ -326,71 +343,79 @@ sra_dkv_kernel(BwdArgs a) {
   const int T = count_steps(sp, it.span_cnt, BQ);
   SpanCursor ld;
   ld.init(sp, it.span_cnt);
-  TileLoader<D, BQ, RQ, kDkvWaves> ql[2], dl;
+  constexpr int NL = kOneStride ? 1 : 2;
+  TileLoader<D, BQ, RQ, kDkvWaves> ql[NL], dl;
 #pragma unroll
-  for (int ss = 0; ss < 2; ++ss) ql[ss].init(a.in_stride[ss], h, wave);
+  for (int ss = 0; ss < NL; ++ss) ql[ss].init(a.in_stride[ss], h, wave);
   dl.init(dstride, h, wave);
-  float lr = 0.f, dr = 0.f;  // wave 0 lanes < BQ stage one row's LSE (log2 units) and delta
-  auto load_row_scalars = [&]() {
-    const int ss = ld.stream();
-    if (wave == 0 && lane < BQ) {
-      const int rr = ld.start() + min(ld.off + lane, ld.len() - 1);
-      lr = a.lse[ss][int64_t(h) * a.rows[ss] + rr] * kLog2e;
-      dr = a.delta[ss][int64_t(h) * a.rows[ss] + rr];
-    }
-  };
-  auto issue_tiles = [&](int b) {
+  // wave 0 lanes < BQ fetch one query row's LSE (log2 units) and delta per step: slot 0 for
+  // even steps, slot 1 for odd ones; they reach LDS at the next barrier
+  float lr[2] = {0.f, 0.f}, dr[2] = {0.f, 0.f};
+  auto issue = [&](int b, int slot) {  // the next step in the cursor -> buffer b
     const int ss = ld.stream();
     if (ld.off + BQ <= ld.len()) {
       const int64_t row0 = int64_t(ld.start() + ld.off);
-      if (ss == 0)
-        ql[0].issue(qs[b], a.q[0] + row0 * a.in_stride[0], wave);
+      if (kOneStride || ss == 0)
+        ql[0].issue(qs[b], a.q[ss] + row0 * a.in_stride[ss], wave);
       else
-        ql[1].issue(qs[b], a.q[1] + row0 * a.in_stride[1], wave);
+        ql[NL - 1].issue(qs[b], a.q[1] + row0 * a.in_stride[1], wave);
       dl.issue(dos[b], a.dout[ss] + row0 * dstride, wave);
     } else {
       tile_load_lds<D, BQ, RQ, kDkvWaves>(qs[b], a.q[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
       tile_load_lds<D, BQ, RQ, kDkvWaves>(dos[b], a.dout[ss], dstride, h, ld.start(), ld.len(), ld.off, wave);
     }
-    load_row_scalars();
+    if (wave == 0 && lane < BQ) {
+      const int rr = ld.start() + min(ld.off + lane, ld.len() - 1);
+      const float l = a.lse[ss][int64_t(h) * a.rows[ss] + rr] * kLog2e;
+      const float d = a.delta[ss][int64_t(h) * a.rows[ss] + rr];
+      if (slot == 0) {
+        lr[0] = l;
+        dr[0] = d;
+      } else {
+        lr[1] = l;
+        dr[1] = d;
+      }
+    }
     ld.advance(BQ);
   };
-  auto stage_scalars = [&](int b) {
+  auto stage = [&](int b, int slot) {
     if (wave == 0 && lane < BQ) {
-      lse_s[b][lane] = lr;
-      dlt_s[b][lane] = dr;
+      lse_s[b][lane] = slot == 0 ? lr[0] : lr[1];
+      dlt_s[b][lane] = slot == 0 ? dr[0] : dr[1];
     }
   };
 
-  issue_tiles(0);
-  stage_scalars(0);
+  issue(0, 0);
+  if (T > 1) issue(1, 1);
   wait_vmem();
+  stage(0, 0);
+  if (T > 1) stage(1, 1);
   __syncthreads();
+  // step t reads buffer t % NB and loads step t + 2 into buffer (t + 2) % NB, whose last
+  // reader (step t - 2) finished before the barrier that ended step t - 1 or t - 2.
+  auto step_tail = [&](int t) {
+    if (t & 1) {  // every odd step: land the loads of steps t + 1 and t + 2, then meet
+      wait_vmem();
+      if (t + 1 < T) stage((t + 1) % NB, (t + 1) & 1);
+      if (t + 2 < T) stage((t + 2) % NB, t & 1);
+      __syncthreads();
+    }
+  };
   int t = 0;
   for (int si = 0; si < it.span_cnt; ++si) {
     const int len = __builtin_amdgcn_readfirstlane(sp[si].len);
     const int full = len / BQ;
     for (int j = 0; j < full; ++j, ++t) {
-      const int b = t & 1;
-      if (t + 1 < T) issue_tiles(b ^ 1);
+      const int b = t % NB;
+      if (t + 2 < T) issue((t + 2) % NB, t & 1);
       if (active) dkv_step<D, false>(st, krow, qs[b], dos[b], lse_s[b], dlt_s[b], BQ, sl2);
-      if (t + 1 < T) {
-        wait_vmem();
-        stage_scalars(b ^ 1);
-      }
-      wait_vmem();
-      __syncthreads();
+      step_tail(t);
     }
     if (len % BQ) {
-      const int b = t & 1;
-      if (t + 1 < T) issue_tiles(b ^ 1);
+      const int b = t % NB;
+      if (t + 2 < T) issue((t + 2) % NB, t & 1);
       if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], lse_s[b], dlt_s[b], len % BQ, sl2);
-      if (t + 1 < T) {
-        wait_vmem();
-        stage_scalars(b ^ 1);
-      }
-      wait_vmem();
-      __syncthreads();
+      step_tail(t);
       ++t;
     }
   }
@@ -415,10 +440,15 @@ sra_dkv_kernel(BwdArgs a) {
 
 hipError_t launch_dkv(const BwdArgs& a, int n_items, int head_dim, hipStream_t stream) {
   if (n_items <= 0) return hipSuccess;
-  if (head_dim == 128)
-    hipLaunchKernelGGL(sra_dkv_kernel<128>, dim3(n_items), dim3(kDkvWaves * 64), 0, stream, a);
-  else
-    hipLaunchKernelGGL(sra_dkv_kernel<64>, dim3(n_items), dim3(kDkvWaves * 64), 0, stream, a);
+  const bool one = a.in_stride[0] == a.in_stride[1];
+  const dim3 grid(n_items), block(kDkvWaves * 64);
+  if (head_dim == 128) {
+    if (one) hipLaunchKernelGGL((sra_dkv_kernel<128, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((sra_dkv_kernel<128, false>), grid, block, 0, stream, a);
+  } else {
+    if (one) hipLaunchKernelGGL((sra_dkv_kernel<64, true>), grid, block, 0, stream, a);
+    else hipLaunchKernelGGL((sra_dkv_kernel<64, false>), grid, block, 0, stream, a);
+  }
   return hipGetLastError();
 }
 
