@@ -8,9 +8,9 @@
 // waves of a SIMD overlap one's softmax (VALU) with the other's matrix products:
 //
 //   S^T (keys x queries) = K Q^T          bf16 MFMA 32x32x16, K rows from LDS, Q^T in VGPRs
-//   online softmax over keys in base 2, lanes = queries (row max/sum are lane-local plus
-//   one permlane32 swap); the running max only moves when it grows by more than 8 (log2),
-//   so rescaling O is rare
+//   online softmax over keys in base 2, lanes = queries (row sums are lane-local plus one
+//   permlane32 swap); the running max is only recomputed when P would exceed 2^16, which
+//   the partial row sums detect, so the common step does no max at all and rescaling is rare
 //   O^T (d x queries) += V^T P^T          V^T fragments via the LDS transpose read
 //
 // Only the last step of a span (its ragged tail) runs the masked variant of the step;
@@ -22,7 +22,7 @@ namespace sra {
 
 namespace {
 constexpr float kLn2 = 0.69314718055994530942f;
-constexpr float kRescaleSlack = 8.0f;  // log2 units: P may grow up to 2^8 before a rescale
+constexpr float kBigSum = 65536.0f;    // a lane's step sum of P above this forces a rescale
 constexpr int kWaves = kFwdQueryTile / 32;
 template <int D> using KTile = PaddedTile<D, kFwdKeyStep, kRowPadRS<D>>;  // row-fragment reads
 template <int D> using VTile = PaddedTile<D, kFwdKeyStep, kTrPadRS<D>>;   // transpose reads
@@ -36,13 +36,15 @@ struct FwdState {
   float l;             // per-lane partial row sum (fp32)
 };
 
-// One 64-key step for the wave's 32 query rows. kMask: keys >= nvalid are outside the span.
+// S^T (keys x queries) of the 64 keys at kt for the wave's 32 query rows; keys >= nvalid are
+// outside the span (kMask).
 template <int D, bool kMask>
-__device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, const __bf16* vt, int nvalid,
-                                         float sl2) {
-  constexpr int NC = D / 16, ND = D / 32;
+__device__ __forceinline__ void fwd_scores(const FwdState<D>& st, const __bf16* kt, int nvalid, floatx16& s0,
+                                           floatx16& s1) {
+  constexpr int NC = D / 16;
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
-  floatx16 s0 = floatx16{}, s1 = floatx16{};  // S^T for keys 0..31 and 32..63
+  s0 = floatx16{};
+  s1 = floatx16{};
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(kt + l32 * kRowPadRS<D> + c * 16 + half * 8);
@@ -58,25 +60,11 @@ __device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, cons
       s1[i] = key + 32 >= nvalid ? -INFINITY : s1[i];
     }
   }
-  // row max as a 4-way tree (short dependency chains)
-  float mq[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) mq[j] = max3f(max2f(s0[4 * j], s1[4 * j]), s0[4 * j + 1], s1[4 * j + 1]);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) mq[j] = max3f(mq[j], s0[4 * j + 2], s1[4 * j + 2]);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) mq[j] = max3f(mq[j], s0[4 * j + 3], s1[4 * j + 3]);
-  const float a = max2f(max2f(mq[0], mq[1]), max2f(mq[2], mq[3]));
-  const float mx = pair_max(a) * sl2;
-  const bool grow = mx > st.m + kRescaleSlack;
-  if (__builtin_expect(__builtin_amdgcn_ballot_w64(grow) != 0, 0)) {
-    const float alpha = grow ? fast_exp2(st.m - mx) : 1.f;
-    st.m = grow ? mx : st.m;
-    st.l *= alpha;
-#pragma unroll
-    for (int db = 0; db < ND; ++db) st.o[db] *= alpha;
-  }
-  const float nm = -st.m;
+}
+
+// P = exp2(S * scale*log2e - m) in place; returns this lane's partial row sum.
+__device__ __forceinline__ float fwd_exp(floatx16& s0, floatx16& s1, float m, float sl2) {
+  const float nm = -m;
   float acc[4] = {0.f, 0.f, 0.f, 0.f};  // 4 independent partial sums
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
@@ -84,7 +72,42 @@ __device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, cons
     s1[i] = fast_exp2(fmaf(s1[i], sl2, nm));
     acc[i & 3] += s0[i] + s1[i];
   }
-  st.l += (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  return (acc[0] + acc[1]) + (acc[2] + acc[3]);
+}
+
+// One 64-key step for the wave's 32 query rows. kMask: keys >= nvalid are outside the span.
+//
+// The running max m is not tracked per step. P is computed against the current m, and its
+// partial row sum doubles as the overflow check: if some lane's 32 values sum to more than
+// kBigSum (some P > kBigSum, or an inf from m = -inf on the first step), the wave takes the
+// rare slow path: recompute S, set m to the true running max, rescale O and l, recompute P.
+// So m always lies within log2(kBigSum) of the true row max, which bounds every P by kBigSum.
+template <int D, bool kMask>
+__device__ __forceinline__ void fwd_step(FwdState<D>& st, const __bf16* kt, const __bf16* vt, int nvalid,
+                                         float sl2) {
+  constexpr int ND = D / 32;
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  floatx16 s0, s1;  // S^T for keys 0..31 and 32..63, then P
+  fwd_scores<D, kMask>(st, kt, nvalid, s0, s1);
+  float lsum = fwd_exp(s0, s1, st.m, sl2);
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(!(lsum <= kBigSum)) != 0, 0)) {
+    fwd_scores<D, kMask>(st, kt, nvalid, s0, s1);
+    float mq[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mq[j] = max3f(max2f(s0[4 * j], s1[4 * j]), s0[4 * j + 1], s1[4 * j + 1]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) mq[j] = max3f(mq[j], max3f(s0[4 * j + 2], s1[4 * j + 2], s0[4 * j + 3]), s1[4 * j + 3]);
+    const float mx = pair_max(max2f(max2f(mq[0], mq[1]), max2f(mq[2], mq[3]))) * sl2;
+    if (mx > st.m) {
+      const float alpha = fast_exp2(st.m - mx);  // 0 when m was -inf
+      st.m = mx;
+      st.l *= alpha;
+#pragma unroll
+      for (int db = 0; db < ND; ++db) st.o[db] *= alpha;
+    }
+    lsum = fwd_exp(s0, s1, st.m, sl2);
+  }
+  st.l += lsum;
   // O^T += V^T P^T: the transpose read gives lane (head dim l32) the 8 keys whose P values
   // the B fragment holds, in the MFMA output's register order.
   const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
