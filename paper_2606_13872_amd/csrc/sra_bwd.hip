@@ -243,11 +243,19 @@ struct DkvState {
 // dK^T += Q^T dS. kMask: query rows >= nvalid are outside the span.
 template <int D, bool kMask>
 __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, const __bf16* qt,
-                                         const __bf16* dt, const float* lse_s, const float* dlt_s,
+                                         const __bf16* dt, const float* lse_s, const float* ndlt_s,
                                          int nvalid, float sl2) {
   constexpr int NC = D / 16, ND = D / 32, RQ = kBothPadRS<D>;
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
-  floatx16 s = floatx16{}, dp = floatx16{};
+  // dP starts from -D (staged negated in LDS, read in the accumulator's row order), so the
+  // MFMAs leave dP - D and dS = P * (dP - D) is one multiply
+  floatx16 s = floatx16{}, dp;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    const floatx4 d4 = *reinterpret_cast<const floatx4*>(ndlt_s + 8 * g + 4 * half);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dp[4 * g + e] = d4[e];
+  }
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qt + l32 * RQ + c * 16 + half * 8);
@@ -260,14 +268,13 @@ __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, co
   for (int g = 0; g < 4; ++g) {
     const int q0 = 8 * g + 4 * half;  // 4 consecutive query rows of this register group
     const floatx4 l4 = *reinterpret_cast<const floatx4*>(lse_s + q0);
-    const floatx4 d4 = *reinterpret_cast<const floatx4*>(dlt_s + q0);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int i = 4 * g + e;
       float p = fast_exp2(fmaf(s[i], sl2, -l4[e]));
       if constexpr (kMask) p = (q0 + e) < nvalid ? p : 0.f;
       s[i] = p;
-      dp[i] = p * (dp[i] - d4[e]);
+      dp[i] = p * dp[i];
     }
   }
   // dV^T += dO^T P and dK^T += Q^T dS ; dO^T and Q^T fragments via the transpose read
@@ -309,7 +316,7 @@ sra_dkv_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(1024))) __bf16 qs[NB][QT::kElems];
   __shared__ __attribute__((aligned(1024))) __bf16 dos[NB][QT::kElems];
   __shared__ __attribute__((aligned(16))) float lse_s[NB][BQ];
-  __shared__ __attribute__((aligned(16))) float dlt_s[NB][BQ];
+  __shared__ __attribute__((aligned(16))) float ndlt_s[NB][BQ];  // -D
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
@@ -367,7 +374,7 @@ sra_dkv_kernel(BwdArgs a) {
     if (wave == 0 && lane < BQ) {
       const int rr = ld.start() + min(ld.off + lane, ld.len() - 1);
       const float l = a.lse[ss][int64_t(h) * a.rows[ss] + rr] * kLog2e;
-      const float d = a.delta[ss][int64_t(h) * a.rows[ss] + rr];
+      const float d = -a.delta[ss][int64_t(h) * a.rows[ss] + rr];  // staged negated
       if (slot == 0) {
         lr[0] = l;
         dr[0] = d;
@@ -381,7 +388,7 @@ sra_dkv_kernel(BwdArgs a) {
   auto stage = [&](int b, int slot) {
     if (wave == 0 && lane < BQ) {
       lse_s[b][lane] = slot == 0 ? lr[0] : lr[1];
-      dlt_s[b][lane] = slot == 0 ? dr[0] : dr[1];
+      ndlt_s[b][lane] = slot == 0 ? dr[0] : dr[1];
     }
   };
 
@@ -408,13 +415,13 @@ sra_dkv_kernel(BwdArgs a) {
     for (int j = 0; j < full; ++j, ++t) {
       const int b = t % NB;
       if (t + 2 < T) issue((t + 2) % NB, t & 1);
-      if (active) dkv_step<D, false>(st, krow, qs[b], dos[b], lse_s[b], dlt_s[b], BQ, sl2);
+      if (active) dkv_step<D, false>(st, krow, qs[b], dos[b], lse_s[b], ndlt_s[b], BQ, sl2);
       step_tail(t);
     }
     if (len % BQ) {
       const int b = t % NB;
       if (t + 2 < T) issue((t + 2) % NB, t & 1);
-      if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], lse_s[b], dlt_s[b], len % BQ, sl2);
+      if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], lse_s[b], ndlt_s[b], len % BQ, sl2);
       step_tail(t);
       ++t;
     }
