@@ -62,6 +62,27 @@ struct PaddedTile {
   static constexpr int kElems = kInstr * 512;                          // LDS elements to reserve
 };
 
+// One GLOBAL_LOAD_LDS_DWORDX4: lane l copies 16 bytes from g to (lds + 16 l); lds is uniform.
+// Issued as inline assembly on purpose: the compiler then does not see an LDS write in
+// flight, and does not stall the LDS reads of the other buffers (which it cannot prove
+// disjoint) until the copy lands. Every reader of a buffer filled this way waits with
+// wait_vmem() and a workgroup barrier first. M0 holds the LDS address for the copy; it is
+// reserved by the compiler, so it is restored right after the instruction has read it.
+__device__ __forceinline__ void lds_dma_x4(const void* g, void* lds) {
+  const uint32_t la = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(la)
+      : "memory");
+}
+
 // Direct global -> LDS copy (gfx950 GLOBAL_LOAD_LDS_DWORDX4) of rows [off, off + NR) of a span
 // into a padded tile. Each wave instruction fills 1 KB of LDS: lane l writes the 16 bytes at
 // (LDS base + 16 l), so lane l fetches the global chunk that belongs there; lanes that land on
@@ -83,8 +104,7 @@ __device__ __forceinline__ void tile_load_lds(__bf16* lds, const __bf16* __restr
       const int ch = slot < CPR ? slot : 0;
       const int rr = min(off + row, len - 1);
       const __bf16* g = src + int64_t(start + rr) * stride + head * D + ch * 8;
-      __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(g),
-                                       (void __attribute__((address_space(3)))*)(lds + ins * 512), 16, 0, 0);
+      lds_dma_x4(g, lds + ins * 512);
     }
   }
 }
@@ -113,8 +133,7 @@ struct TileLoader {
     for (int j = 0; j < kSlots; ++j) {
       const int ins = wave + j * NW;
       if (ins < TL::kInstr)
-        __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(first_row + voff[j]),
-                                         (void __attribute__((address_space(3)))*)(lds + ins * 512), 16, 0, 0);
+        lds_dma_x4(first_row + voff[j], lds + ins * 512);
     }
   }
 };
