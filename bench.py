@@ -309,6 +309,21 @@ def main():
         "bwd_tflops": round(bwd_flops / (ms_bwd * 1e-3) / 1e12, 2) if ms_bwd else None,
         "roofline": roofline,
     }
+    # reference as cached context only (the denoising-step path): gen rows alone
+    go_out = {"o_gen": fo["o_gen"], "lse_gen": fo["lse_gen"], "workspace": fo["workspace"]}
+    sra.forward(ins[0], ins[1], ins[2], None, ins[4], ins[5], w.samples, out=go_out, gen_queries_only=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        sra.forward(ins[0], ins[1], ins[2], None, ins[4], ins[5], w.samples, out=go_out, gen_queries_only=True)
+    e1.record()
+    torch.cuda.synchronize()
+    go_ms = e0.elapsed_time(e1) / args.steps
+    go_pairs, _ = sra.pair_counts(w.samples, H, d, flags=sra.FLAG_GEN_QUERIES_ONLY)
+    line["gen_queries_only_fwd"] = {"ms": round(go_ms, 3),
+                                    "tflops": round(4 * d * go_pairs * H / (go_ms * 1e-3) / 1e12, 2)}
+    print(f"[bench] gen-only forward {go_ms:.2f} ms", file=sys.stderr, flush=True)
     if args.cpu_rows > 0:
         print("[bench] cpu oracle sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = _cpu_baseline(x, w, args.cpu_rows, torch)

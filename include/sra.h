@@ -68,8 +68,18 @@ typedef struct sra_problem {
   const sra_sample_geom* samples;    /* host array [batch]                                     */
   int64_t gen_token_stride;          /* elements between gen q/k/v tokens; 0 selects H*d       */
   int64_t ref_token_stride;          /* elements between ref q/k/v tokens; 0 selects H*d       */
-  uint32_t flags;                    /* must be 0 (reserved)                                   */
+  uint32_t flags;                    /* 0 or SRA_FLAG_* bits                                   */
 } sra_problem;
+
+/* Problem flags.
+ * SRA_FLAG_GEN_QUERIES_ONLY: reference tokens are context only, not queries. This is the
+ *   inference path of cached reference K/V (§4.3): across denoising steps the reference
+ *   tokens' own outputs do not change, so only the generation rows are computed. The
+ *   forward writes o_gen and lse_gen only; q_ref, o_ref and lse_ref are not read or written
+ *   and may be NULL. The backward is that of the gen rows alone (equivalently: do_ref = 0):
+ *   it writes dq_gen, dk_gen, dv_gen, dk_ref and dv_ref; q_ref, o_ref, lse_ref, do_ref and
+ *   dq_ref are not touched and may be NULL. Pair counts and schedules omit the ref queries. */
+enum { SRA_FLAG_GEN_QUERIES_ONLY = 1u };
 
 /* Which schedule an inspection hook looks at. */
 enum {

@@ -48,13 +48,14 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
     return p->head_dim > 0 ? SRA_ERR_UNSUPPORTED : SRA_ERR_INVALID_ARGUMENT;
   }
   if (!p->samples) { *err = "samples is NULL"; return SRA_ERR_INVALID_ARGUMENT; }
-  if (p->flags != 0) { *err = "flags must be 0"; return SRA_ERR_INVALID_ARGUMENT; }
+  if (p->flags & ~uint32_t(SRA_FLAG_GEN_QUERIES_ONLY)) { *err = "unknown flag bits"; return SRA_ERR_INVALID_ARGUMENT; }
   if (!(std::isfinite(p->softmax_scale))) { *err = "softmax_scale is not finite"; return SRA_ERR_INVALID_ARGUMENT; }
   const int64_t hd = int64_t(p->num_heads) * p->head_dim;
   Layout L;
   L.batch = p->batch;
   L.heads = p->num_heads;
   L.head_dim = p->head_dim;
+  L.gen_only = (p->flags & SRA_FLAG_GEN_QUERIES_ONLY) != 0;
   L.scale = p->softmax_scale > 0.f ? p->softmax_scale : float(1.0 / std::sqrt(double(p->head_dim)));
   L.gen_stride = p->gen_token_stride == 0 ? hd : p->gen_token_stride;
   L.ref_stride = p->ref_token_stride == 0 ? hd : p->ref_token_stride;
@@ -115,7 +116,7 @@ void closed_form_pairs(const Layout& L, int64_t* gen_pairs, int64_t* ref_pairs) 
     }
   }
   if (gen_pairs) *gen_pairs = gp;
-  if (ref_pairs) *ref_pairs = rp;
+  if (ref_pairs) *ref_pairs = L.gen_only ? 0 : rp;
 }
 
 namespace {
@@ -187,6 +188,7 @@ void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
       s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
     c.span_cnt = int32_t(s->spans.size()) - c.span_off;
     classes.push_back(c);
+    if (L.gen_only) continue;
     // ref queries: per group, keys = valid runs of the group; query tiles per valid run
     for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
       std::vector<Run> runs = valid_runs(sm, g0, std::min(sm.ref_frames, g0 + sm.group));
@@ -219,10 +221,12 @@ void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
       if (runs.empty()) continue;
       int32_t off = int32_t(s->spans.size());
       s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
+      if (!L.gen_only)
+        for (const Run& r : runs)
+          s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
+      const int32_t cnt = int32_t(s->spans.size()) - off;
       for (const Run& r : runs)
-        s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
-      for (const Run& r : runs)
-        classes.push_back({1, sm.ref_off + r.f0 * sm.F, (r.f1 - r.f0) * sm.F, off, int32_t(runs.size()) + 1, b, 0});
+        classes.push_back({1, sm.ref_off + r.f0 * sm.F, (r.f1 - r.f0) * sm.F, off, cnt, b, 0});
     }
   }
   std::vector<std::pair<int64_t, WorkItem>> v;
@@ -264,7 +268,7 @@ int64_t covered_pairs(const Schedule& s, bool /*key_major*/) {
 std::string layout_key(const Layout& L) {
   std::string k;
   auto put = [&k](int64_t v) { k.append(reinterpret_cast<const char*>(&v), sizeof v); };
-  put(L.batch); put(L.heads); put(L.head_dim);
+  put(L.batch); put(L.heads); put(L.head_dim); put(L.gen_only ? 1 : 0);
   for (const SampleLayout& s : L.samples) {
     put(s.G); put(s.R); put(s.F); put(s.ref_frames); put(s.group);
     k.append(reinterpret_cast<const char*>(s.valid.data()), s.valid.size());

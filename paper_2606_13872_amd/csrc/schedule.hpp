@@ -24,6 +24,7 @@ struct Layout {
   float scale = 0.f;
   int64_t gen_stride = 0, ref_stride = 0;  // q/k/v token strides (elements)
   int64_t sum_gen = 0, sum_ref = 0;
+  bool gen_only = false;                   // SRA_FLAG_GEN_QUERIES_ONLY: no reference queries
   std::vector<SampleLayout> samples;
 };
 

@@ -267,7 +267,8 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
   std::shared_ptr<CachedPlan> cp;
   sra_status st = common_checks(p, &L, &cp);
   if (st != SRA_OK) return st;
-  st = check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen}, {q_ref, k_ref, v_ref, o_ref, lse_ref});
+  st = L.gen_only ? check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen}, {k_ref, v_ref})
+                  : check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen}, {q_ref, k_ref, v_ref, o_ref, lse_ref});
   if (st != SRA_OK) return st;
   const size_t need = fwd_workspace(*cp);
   if (workspace_bytes < need)
@@ -306,7 +307,7 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
   a.scale_log2 = float(double(L.scale) * 1.4426950408889634);
   hipError_t e = timed(SRA_KERNEL_FORWARD, s, [&] { return launch_forward(a, int(P.fwd.items.size()), L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "forward launch");
-  if (!P.fill.empty()) {
+  if (!P.fill.empty() && !L.gen_only) {  // ref rows of invalid frames (no ref rows when gen-only)
     FillArgs f{};
     f.ranges = reinterpret_cast<const FillRange*>(ws + cp->fwd.offsets[2]);
     f.n_ranges = int32_t(P.fill.size());
@@ -331,8 +332,10 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
   std::shared_ptr<CachedPlan> cp;
   sra_status st = common_checks(p, &L, &cp);
   if (st != SRA_OK) return st;
-  st = check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen, do_gen, dq_gen, dk_gen, dv_gen},
-                     {q_ref, k_ref, v_ref, o_ref, lse_ref, do_ref, dq_ref, dk_ref, dv_ref});
+  st = L.gen_only ? check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen, do_gen, dq_gen, dk_gen, dv_gen},
+                                  {k_ref, v_ref, dk_ref, dv_ref})
+                  : check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen, do_gen, dq_gen, dk_gen, dv_gen},
+                                  {q_ref, k_ref, v_ref, o_ref, lse_ref, do_ref, dq_ref, dk_ref, dv_ref});
   if (st != SRA_OK) return st;
   const size_t need = bwd_workspace(*cp, L);
   if (workspace_bytes < need)
@@ -358,7 +361,7 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
   d.delta[0] = delta_gen;
   d.delta[1] = delta_ref;
   d.rows[0] = int32_t(L.sum_gen);
-  d.rows[1] = int32_t(L.sum_ref);
+  d.rows[1] = L.gen_only ? 0 : int32_t(L.sum_ref);  // no ref query rows when gen-only
   d.heads = L.heads;
   e = timed(SRA_KERNEL_DELTA, s, [&] { return launch_delta(d, L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "delta launch");
@@ -405,7 +408,7 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
     f.n_ranges = int32_t(P.fill.size());
     f.heads = L.heads;
     f.head_dim = L.head_dim;
-    f.t[0] = static_cast<__bf16*>(dq_ref);
+    f.t[0] = L.gen_only ? nullptr : static_cast<__bf16*>(dq_ref);
     f.t[1] = static_cast<__bf16*>(dk_ref);
     f.t[2] = static_cast<__bf16*>(dv_ref);
     e = timed(SRA_KERNEL_FILL, s, [&] { return launch_fill(f, s); });

@@ -97,6 +97,9 @@ def status_string(status: int) -> str:
         return f"status {status}"
 
 
+FLAG_GEN_QUERIES_ONLY = 1  # SRA_FLAG_GEN_QUERIES_ONLY: reference tokens are context only
+
+
 def _check(status: int) -> None:
     if status != SRA_OK:
         raise SRAError(status, lib().sra_last_error().decode())
@@ -143,24 +146,24 @@ class Problem:
 
 
 # ----------------------------------------------------------------------------- host hooks
-def pair_counts(samples, heads=1, head_dim=128) -> Tuple[int, int]:
-    p = Problem(samples, heads, head_dim)
+def pair_counts(samples, heads=1, head_dim=128, flags=0) -> Tuple[int, int]:
+    p = Problem(samples, heads, head_dim, flags=flags)
     g, r = ctypes.c_int64(0), ctypes.c_int64(0)
     _check(lib().sra_pair_counts(p.ptr, ctypes.byref(g), ctypes.byref(r)))
     return int(g.value), int(r.value)
 
 
-def schedule_info(samples, which: int, heads=1, head_dim=128) -> Tuple[int, int, int]:
-    p = Problem(samples, heads, head_dim)
+def schedule_info(samples, which: int, heads=1, head_dim=128, flags=0) -> Tuple[int, int, int]:
+    p = Problem(samples, heads, head_dim, flags=flags)
     a, b, c = ctypes.c_int64(0), ctypes.c_int64(0), ctypes.c_int64(0)
     _check(lib().sra_schedule_info(p.ptr, which, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)))
     return int(a.value), int(b.value), int(c.value)
 
 
-def schedule_mask(samples, which: int, sample: int, heads=1, head_dim=128):
+def schedule_mask(samples, which: int, sample: int, heads=1, head_dim=128, flags=0):
     import numpy as np
 
-    p = Problem(samples, heads, head_dim)
+    p = Problem(samples, heads, head_dim, flags=flags)
     g = p.samples[sample]
     n = g.gen_frames * g.gen_h * g.gen_w + g.ref_frames * g.ref_h * g.ref_w
     out = np.zeros((n, n), dtype=np.uint8)
@@ -168,11 +171,11 @@ def schedule_mask(samples, which: int, sample: int, heads=1, head_dim=128):
     return out
 
 
-def schedule_export(samples, which: int, heads=1, head_dim=128):
+def schedule_export(samples, which: int, heads=1, head_dim=128, flags=0):
     import numpy as np
 
-    n_items, n_spans, _ = schedule_info(samples, which, heads, head_dim)
-    p = Problem(samples, heads, head_dim)
+    n_items, n_spans, _ = schedule_info(samples, which, heads, head_dim, flags)
+    p = Problem(samples, heads, head_dim, flags=flags)
     items = np.zeros((n_items, 8), dtype=np.int32)
     spans = np.zeros((n_spans, 4), dtype=np.int32)
     _check(lib().sra_schedule_export(p.ptr, which, items.ctypes.data_as(ctypes.c_void_p), items.size,
@@ -234,24 +237,32 @@ def _alloc_workspace(nbytes, device):
 
 
 def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[float] = None,
-            out: Optional[Dict] = None):
-    """SRA forward on the GPU. Returns (o_gen, o_ref, lse_gen, lse_ref)."""
+            out: Optional[Dict] = None, gen_queries_only: bool = False):
+    """SRA forward on the GPU. Returns (o_gen, o_ref, lse_gen, lse_ref).
+
+    gen_queries_only: the reference tokens are context only (cached reference K/V); only the
+    generation rows are computed, q_ref may be None and o_ref / lse_ref are returned as None.
+    """
     import torch
 
     H, d = q_gen.shape[1], q_gen.shape[2]
     dev = q_gen.device
+    go = bool(gen_queries_only)
     p = Problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
-                _token_stride([q_ref, k_ref, v_ref], "ref"))
+                _token_stride([None if go else q_ref, k_ref, v_ref], "ref"), FLAG_GEN_QUERIES_ONLY if go else 0)
     for t in (q_gen, k_gen, v_gen, q_ref, k_ref, v_ref):
         if t is not None and t.dtype != torch.bfloat16:
             raise TypeError("q/k/v must be bfloat16")
-    if q_gen.shape[0] != p.n_gen or (q_ref is not None and q_ref.shape[0] != p.n_ref):
+    if q_gen.shape[0] != p.n_gen or (k_ref is not None and k_ref.shape[0] != p.n_ref):
         raise ValueError("token counts do not match the geometry")
     out = out or {}
     o_gen = out.get("o_gen", torch.empty((p.n_gen, H, d), dtype=torch.bfloat16, device=dev))
-    o_ref = out.get("o_ref", torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
     lse_gen = out.get("lse_gen", torch.empty((H, p.n_gen), dtype=torch.float32, device=dev))
-    lse_ref = out.get("lse_ref", torch.empty((H, p.n_ref), dtype=torch.float32, device=dev))
+    if go:
+        q_ref = o_ref = lse_ref = None
+    else:
+        o_ref = out.get("o_ref", torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
+        lse_ref = out.get("lse_ref", torch.empty((H, p.n_ref), dtype=torch.float32, device=dev))
     nbytes = p.workspace_size(False)
     ws = out.get("workspace")
     if ws is None or ws.numel() < nbytes:
@@ -263,14 +274,21 @@ def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[f
 
 
 def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, lse_ref, do_gen, do_ref,
-             samples, scale: Optional[float] = None, out: Optional[Dict] = None):
-    """SRA backward on the GPU. Returns dict dq_gen, dk_gen, dv_gen, dq_ref, dk_ref, dv_ref."""
+             samples, scale: Optional[float] = None, out: Optional[Dict] = None, gen_queries_only: bool = False):
+    """SRA backward on the GPU. Returns dict dq_gen, dk_gen, dv_gen, dq_ref, dk_ref, dv_ref.
+
+    gen_queries_only: gradients of the generation rows alone (reference tokens are context
+    only); q_ref, o_ref, lse_ref and do_ref may be None and dq_ref is returned as None.
+    """
     import torch
 
     H, d = q_gen.shape[1], q_gen.shape[2]
     dev = q_gen.device
+    go = bool(gen_queries_only)
+    if go:
+        q_ref = o_ref = lse_ref = do_ref = None
     p = Problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
-                _token_stride([q_ref, k_ref, v_ref], "ref"))
+                _token_stride([q_ref, k_ref, v_ref], "ref"), FLAG_GEN_QUERIES_ONLY if go else 0)
     for t in (o_gen, o_ref, do_gen, do_ref):
         if t is not None and t.numel() and not t.is_contiguous():
             raise ValueError("o and do must be dense [tokens, heads, head_dim]")
@@ -279,7 +297,8 @@ def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, ls
     for n in ("dq_gen", "dk_gen", "dv_gen"):
         g[n] = out.get(n, torch.empty((p.n_gen, H, d), dtype=torch.bfloat16, device=dev))
     for n in ("dq_ref", "dk_ref", "dv_ref"):
-        g[n] = out.get(n, torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
+        g[n] = None if (go and n == "dq_ref") else \
+            out.get(n, torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
     nbytes = p.workspace_size(True)
     ws = out.get("workspace")
     if ws is None or ws.numel() < nbytes:

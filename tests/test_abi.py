@@ -49,10 +49,12 @@ def test_invalid_problems_are_rejected(samples, heads, d, stride, status):
 
 
 def test_flags_and_batch_validation():
-    p = sra.Problem(GOOD, 1, 64, flags=1)
-    with pytest.raises(sra.SRAError) as e:
-        p.workspace_size(False)
-    assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+    for bad in (2, 4, 0x80000000, 3):
+        p = sra.Problem(GOOD, 1, 64, flags=bad)
+        with pytest.raises(sra.SRAError) as e:
+            p.workspace_size(False)
+        assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+    assert sra.Problem(GOOD, 1, 64, flags=sra.FLAG_GEN_QUERIES_ONLY).workspace_size(False) > 0
     p = sra.Problem([], 1, 64)
     with pytest.raises(sra.SRAError):
         p.workspace_size(False)
@@ -94,3 +96,10 @@ def test_backward_rejects_small_workspace():
     st = sra.lib().sra_backward(p.ptr, *([fake] * 18), fake, ctypes.c_size_t(p.workspace_size(True) - 256),
                                 ctypes.c_void_p(0))
     assert st == sra.SRA_ERR_WORKSPACE_TOO_SMALL
+
+
+def test_flag_constant_matches_the_header():
+    import re
+    text = open(sra.HEADER_PATH).read()
+    m = re.search(r"SRA_FLAG_GEN_QUERIES_ONLY\s*=\s*(\d+)u", text)
+    assert m and int(m.group(1)) == sra.FLAG_GEN_QUERIES_ONLY

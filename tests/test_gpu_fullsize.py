@@ -208,3 +208,14 @@ def test_fullsize_reference_frames_with_zero_gen_upstream():
             for n, want in (("dq_ref", dq), ("dk_ref", dk), ("dv_ref", dv)):
                 got = g[n][fr, h].double().cpu().numpy()
                 _close(f"{n} h{h} f{f}", got, want)
+
+
+def test_fullsize_gen_queries_only_forward_is_the_gen_half():
+    """720p with the reference as cached context only: bitwise the gen rows of the full call."""
+    w = workload("720p")
+    x = _inputs(w, grads=False)
+    full = sra.forward(*[x[k] for k in INS], w.samples)
+    go = sra.forward(x["q_gen"], x["k_gen"], x["v_gen"], None, x["k_ref"], x["v_ref"], w.samples,
+                     gen_queries_only=True)
+    torch.cuda.synchronize()
+    assert torch.equal(go[0], full[0]) and torch.equal(go[2], full[2])

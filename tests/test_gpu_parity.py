@@ -268,3 +268,51 @@ def test_error_paths_do_not_launch():
     assert torch.all(o["o_gen"].float() == 7.0)
     with pytest.raises(ValueError):
         sra.forward(y["q_gen"][:10], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], samples)
+
+
+# ------------------------------------------------------------------- reference as context only
+GEN_ONLY_CASES = {
+    "invalid_groups": [SampleGeom(2, 12, 13, 6, 5, 7, group_frames=2, frame_valid=[1, 0, 1, 1, 0, 0])],
+    "varlen": [SampleGeom(2, 9, 15, 2, 9, 15), SampleGeom(1, 11, 7, 5, 6, 6), SampleGeom(1, 5, 5, 0, 3, 3)],
+}
+
+
+@pytest.mark.parametrize("case", list(GEN_ONLY_CASES))
+def test_gen_queries_only_forward_is_the_gen_half(case):
+    """Cached reference K/V (§4.3): the gen-only forward equals the gen rows of the full
+    forward bitwise (same schedule for those rows) and the oracle's gen rows."""
+    samples, H, d = GEN_ONLY_CASES[case], 2, 128
+    x = make_inputs(samples, H, d, 31)
+    y = {k: v.cuda() for k, v in x.items()}
+    full = sra.forward(y["q_gen"], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], samples)
+    go = sra.forward(y["q_gen"], y["k_gen"], y["v_gen"], None, y["k_ref"], y["v_ref"], samples,
+                     gen_queries_only=True)
+    torch.cuda.synchronize()
+    assert go[1] is None and go[3] is None
+    assert torch.equal(go[0], full[0]) and torch.equal(go[2], full[2])
+    o_gen, _, lse_gen, _ = oracle.sra_forward({k: to_numpy64(v) for k, v in x.items()}, samples)
+    assert_close("o_gen", go[0], o_gen, 1)
+    assert_lse("lse_gen", go[2], lse_gen)
+
+
+@pytest.mark.parametrize("case", list(GEN_ONLY_CASES))
+def test_gen_queries_only_backward_is_zero_reference_upstream(case):
+    """The gen-only backward equals the full backward with do_ref = 0 (bitwise: the reference
+    queries then add exact zeros) and the oracle's gradients for that upstream; dq_ref is
+    not produced."""
+    samples, H, d = GEN_ONLY_CASES[case], 2, 128
+    x = make_inputs(samples, H, d, 32)
+    x["do_ref"].zero_()
+    y = {k: v.cuda() for k, v in x.items()}
+    ins = [y[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
+    o = sra.forward(*ins, samples)
+    full = sra.backward(*ins, *o, y["do_gen"], y["do_ref"], samples)
+    go = sra.backward(y["q_gen"], y["k_gen"], y["v_gen"], None, y["k_ref"], y["v_ref"], o[0], None, o[2], None,
+                      y["do_gen"], None, samples, gen_queries_only=True)
+    torch.cuda.synchronize()
+    assert go["dq_ref"] is None
+    for n in ("dq_gen", "dk_gen", "dv_gen", "dk_ref", "dv_ref"):
+        assert torch.equal(go[n], full[n]), n
+    want = oracle.sra_backward({k: to_numpy64(v) for k, v in x.items()}, samples)
+    for n in ("dq_gen", "dk_gen", "dv_gen", "dk_ref", "dv_ref"):
+        assert_close(n, go[n], want[n], 1)

@@ -53,6 +53,22 @@ def test_pair_counts_closed_form_equals_mask(gi):
         assert covered == total
 
 
+@pytest.mark.parametrize("gi", range(len(GEOMS)))
+@pytest.mark.parametrize("which", SCHEDS)
+def test_gen_queries_only_schedules_drop_exactly_the_reference_rows(gi, which):
+    """With reference tokens as context only (cached reference K/V, §4.3), every schedule
+    covers exactly the gen rows of the visibility mask and no reference query row."""
+    samples = GEOMS[gi]
+    for b, g in enumerate(samples):
+        want = oracle.visibility_mask(g).astype(np.uint8)
+        want[g.n_gen:, :] = 0
+        got = sra.schedule_mask(samples, which, b, flags=sra.FLAG_GEN_QUERIES_ONLY)
+        assert np.array_equal(got, want), (which, b, np.argwhere(got != want)[:5])
+    gp, rp = oracle.pair_counts(samples)
+    assert sra.pair_counts(samples, flags=sra.FLAG_GEN_QUERIES_ONLY) == (gp, 0)
+    assert sra.schedule_info(samples, which, flags=sra.FLAG_GEN_QUERIES_ONLY)[2] == gp
+
+
 def _golden():
     with open(os.path.join(os.path.dirname(__file__), "golden", "pair_counts.json")) as f:
         return json.load(f)
