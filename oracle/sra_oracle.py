@@ -63,7 +63,10 @@ def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
     """Explicit visibility mask of one sample, rows and columns in [gen ; ref] order.
 
     M[q, k] is True when query q may attend to key k:
-      gen q, gen k : True                               (full base self-attention)
+      gen q, gen k : True                               (full base self-attention), or
+                     |gframe(q) - gframe(k)| <= w when the sample has gen_window = w
+                     (§2.4: the refiner's sparse temporal attention keeps each frame's
+                     receptive field to a local neighbourhood of latent frames)
       gen q, ref k : valid(frame(k))                    (§1: gen sees every reference token)
       ref q, gen k : False                              (§1, §8.2: reference attends only within itself)
       ref q, ref k : valid(frame(q)) and valid(frame(k)) and group(q) == group(k)
@@ -82,7 +85,15 @@ def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
     key_valid = v[key_frame] if R > 0 else np.zeros(0, dtype=bool)
     key_group = key_frame // g
     # generation query rows
-    M[is_gen, :G] = True
+    w = getattr(geom, "gen_window", None)
+    if w is None:
+        M[is_gen, :G] = True
+    else:
+        assert w >= 0
+        Fg = geom.gen_h * geom.gen_w
+        q_gframe = rows[is_gen] // Fg
+        k_gframe = np.arange(G) // Fg
+        M[np.ix_(np.nonzero(is_gen)[0], np.arange(G))] = np.abs(q_gframe[:, None] - k_gframe[None, :]) <= w
     M[np.ix_(is_gen, np.arange(G, G + R))] = key_valid[None, :]
     # reference query rows
     ref_rows = np.nonzero(~is_gen)[0]

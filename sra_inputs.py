@@ -15,6 +15,8 @@ Workload recipes (the paper gives no SRA workload; these mirror its video shapes
   * varlen  : 4 samples, gen 5x68x120 = 40,800 each, ref {4,2,8,4} x 68x120 frames, H=24,
               d=128, seed 4, RMS Q/K. The reference lengths are drawn once from
               numpy default_rng(13872).choice([2, 4, 8, 12], 4).
+  * varlen_window : the varlen batch with a +-1 latent-frame window on gen-gen attention
+              (the refiner's sparse temporal attention), seed 5.
 Every value is an iid N(0,1) fp32 draw rounded to bf16 (round-to-nearest-even).
 Draw order: q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, do_gen, do_ref.
 """
@@ -33,7 +35,9 @@ class SampleGeom:
     gen_frames x gen_h x gen_w generation tokens, ref_frames x ref_h x ref_w reference
     tokens. group_frames consecutive reference latent frames form one self-attention
     group of reference queries. frame_valid (None = all valid) marks reference frames
-    that take part at all (e.g. frames where the face is visible).
+    that take part at all (e.g. frames where the face is visible). gen_window (None = no
+    window) limits which generation keys a generation query sees to the latent frames within
+    that many frames of its own (the refiner's sparse temporal attention).
     """
 
     gen_frames: int
@@ -44,6 +48,7 @@ class SampleGeom:
     ref_w: int
     group_frames: int = 1
     frame_valid: Optional[Sequence[int]] = field(default=None)
+    gen_window: Optional[int] = None
 
     @property
     def n_gen(self) -> int:
@@ -80,6 +85,10 @@ def workload(name: str) -> Workload:
     if name == "varlen":
         return Workload(name, [SampleGeom(5, 68, 120, r, 68, 120) for r in VARLEN_REF_FRAMES],
                         24, 128, 4, True)
+    if name == "varlen_window":
+        # the same packed batch with the refiner's temporal window: +-1 latent frame
+        return Workload(name, [SampleGeom(5, 68, 120, r, 68, 120, gen_window=1) for r in VARLEN_REF_FRAMES],
+                        24, 128, 5, True)
     raise KeyError(name)
 
 

@@ -68,9 +68,33 @@ def mask_ignores_validity(geom, rows=None):
     class G2:
         pass
     g = G2()
-    for k in ("gen_frames", "gen_h", "gen_w", "ref_frames", "ref_h", "ref_w", "group_frames"):
+    for k in ("gen_frames", "gen_h", "gen_w", "ref_frames", "ref_h", "ref_w", "group_frames", "gen_window"):
         setattr(g, k, getattr(geom, k))
     g.frame_valid = None
+    return _orig_mask(g, rows)
+
+
+def mask_window_strict(geom, rows=None):
+    # off by one: |frame difference| < w instead of <= w
+    w = getattr(geom, "gen_window", None)
+    if w is None:
+        return _orig_mask(geom, rows)
+    M = _orig_mask(geom, rows)
+    G, fg = geom.n_gen, geom.gen_h * geom.gen_w
+    r = np.arange(G + geom.n_ref) if rows is None else np.asarray(rows)
+    for i, q in enumerate(r):
+        if q < G:
+            M[i, :G] &= np.abs(q // fg - np.arange(G) // fg) < w
+    return M
+
+
+def mask_window_ignored(geom, rows=None):
+    class G2:
+        pass
+    g = G2()
+    for k in ("gen_frames", "gen_h", "gen_w", "ref_frames", "ref_h", "ref_w", "group_frames", "frame_valid"):
+        setattr(g, k, getattr(geom, k))
+    g.gen_window = None
     return _orig_mask(g, rows)
 
 
@@ -115,7 +139,11 @@ def _all_forward_pins():
         pins.test_gen_rows_equal_dense_attention_over_gen_and_valid_ref(geom)
         pins.test_ref_rows_equal_per_group_dense_attention(geom)
         pins.test_zero_keys_give_log_visible_count(geom)
-    pins.test_brute_force_quadruple_loop(2)
+    pins.test_brute_force_quadruple_loop(2, None)
+    pins.test_brute_force_quadruple_loop(1, 0)
+    pins.test_brute_force_quadruple_loop(2, 1)
+    pins.test_window_zero_without_reference_is_per_frame_attention()
+    pins.test_window_pair_count_closed_form()
 
 
 def _all_backward_pins():
@@ -129,6 +157,8 @@ def _all_backward_pins():
     ("visibility_mask", mask_ref_sees_all_ref, "fwd"),
     ("visibility_mask", mask_group_modulo, "fwd"),
     ("visibility_mask", mask_ignores_validity, "fwd"),
+    ("visibility_mask", mask_window_strict, "fwd"),
+    ("visibility_mask", mask_window_ignored, "fwd"),
     ("attention_rows", rows_no_scale, "fwd"),
     ("attention_rows", rows_lse_without_max, "fwd"),
     ("attention_backward_full", bwd_sign, "bwd"),

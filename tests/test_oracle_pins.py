@@ -34,7 +34,11 @@ def pred_visible(geom, qi, ki):
     valid = [True] * geom.ref_frames if geom.frame_valid is None else [bool(x) for x in geom.frame_valid]
     q_is_gen, k_is_gen = qi < G, ki < G
     if q_is_gen and k_is_gen:
-        return True
+        w = getattr(geom, "gen_window", None)
+        if w is None:
+            return True
+        fg = geom.gen_h * geom.gen_w
+        return abs(qi // fg - ki // fg) <= w
     if q_is_gen:
         return valid[(ki - G) // F]
     if k_is_gen:
@@ -48,7 +52,11 @@ def visible_count_closed_form(geom, qi):
     F = geom.ref_h * geom.ref_w
     valid = [True] * geom.ref_frames if geom.frame_valid is None else [bool(x) for x in geom.frame_valid]
     if qi < G:
-        return G + F * sum(valid)
+        w = getattr(geom, "gen_window", None)
+        if w is None:
+            return G + F * sum(valid)
+        t, T = qi // (geom.gen_h * geom.gen_w), geom.gen_frames
+        return (min(T - 1, t + w) - max(0, t - w) + 1) * geom.gen_h * geom.gen_w + F * sum(valid)
     f = (qi - G) // F
     if not valid[f]:
         return 0
@@ -185,7 +193,7 @@ def test_one_hot_values_recover_the_mask(geom):
 
 
 def test_mask_equals_predicates_and_pair_counts_close():
-    for geom in GEOMS + [SampleGeom(2, 3, 3, 7, 2, 2, group_frames=3, frame_valid=[0, 1, 1, 0, 1, 1, 1])]:
+    for geom in GEOMS + [SampleGeom(2, 3, 3, 7, 2, 2, group_frames=3, frame_valid=[0, 1, 1, 0, 1, 1, 1])] + WINDOW_GEOMS:
         M = oracle.visibility_mask(geom)
         n = geom.n_gen + geom.n_ref
         P = np.array([[pred_visible(geom, i, j) for j in range(n)] for i in range(n)])
@@ -282,9 +290,9 @@ def test_asymmetry_gen_inputs_never_reach_reference_outputs(geom):
 
 
 # --------------------------------------------------------------------- brute force
-@pytest.mark.parametrize("g", [1, 2, 3])
-def test_brute_force_quadruple_loop(g):
-    geom = SampleGeom(2, 2, 2, 3, 2, 2, group_frames=g, frame_valid=[1, 0, 1])
+@pytest.mark.parametrize("g,w", [(1, None), (2, None), (3, None), (1, 0), (2, 1)])
+def test_brute_force_quadruple_loop(g, w):
+    geom = SampleGeom(3, 2, 2, 3, 2, 2, group_frames=g, frame_valid=[1, 0, 1], gen_window=w)
     H, d = 2, 4
     x = rand_inputs([geom], H, d)
     o_gen, o_ref, lse_gen, lse_ref = oracle.sra_forward(x, [geom])
@@ -409,3 +417,53 @@ def test_float32_mode_tracks_float64():
     for u, v in zip(a, b):
         fin = np.isfinite(u)
         assert np.abs(u[fin] - v[fin]).max() < 1e-5
+
+
+# --------------------------------------------------------------- refiner temporal window
+# §2.4: the refiner keeps each frame's receptive field to a local temporal neighbourhood; its
+# width is a parameter (gen_window latent frames on each side); gen queries still see the full
+# valid reference.
+WINDOW_GEOMS = [
+    SampleGeom(4, 2, 3, 2, 2, 2, gen_window=0),
+    SampleGeom(5, 2, 2, 3, 2, 2, frame_valid=[1, 0, 1], gen_window=1),
+    SampleGeom(3, 3, 2, 0, 1, 1, gen_window=1),
+    SampleGeom(6, 1, 3, 4, 1, 3, group_frames=2, gen_window=2),
+]
+
+
+def test_window_covering_every_frame_is_full_attention():
+    base = SampleGeom(4, 3, 2, 3, 2, 2, frame_valid=[1, 1, 0])
+    wide = SampleGeom(4, 3, 2, 3, 2, 2, frame_valid=[1, 1, 0], gen_window=3)
+    assert np.array_equal(oracle.visibility_mask(base), oracle.visibility_mask(wide))
+    x = rand_inputs([base], 2, 8)
+    a, b = oracle.sra_forward(x, [base]), oracle.sra_forward(x, [wide])
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+
+
+def test_window_zero_without_reference_is_per_frame_attention():
+    """w = 0 and R = 0: every generation frame attends only to itself (dense SDPA per frame)."""
+    geom = SampleGeom(3, 2, 3, 0, 1, 1, gen_window=0)
+    H, d = 2, 8
+    x = rand_inputs([geom], H, d)
+    o_gen, _, lse_gen, _ = oracle.sra_forward(x, [geom])
+    fg = geom.gen_h * geom.gen_w
+    for t in range(geom.gen_frames):
+        sl = slice(t * fg, (t + 1) * fg)
+        for h in range(H):
+            q, k, v = (torch.tensor(x[n][sl, h]) for n in ("q_gen", "k_gen", "v_gen"))
+            o = torch.nn.functional.scaled_dot_product_attention(q[None], k[None], v[None], scale=1 / math.sqrt(d))[0]
+            np.testing.assert_allclose(o_gen[sl, h], o.numpy(), rtol=1e-12, atol=1e-13)
+            s = (q @ k.T).numpy() / math.sqrt(d)
+            m = s.max(axis=1)
+            np.testing.assert_allclose(lse_gen[h, sl], m + np.log(np.exp(s - m[:, None]).sum(axis=1)), rtol=1e-12)
+
+
+def test_window_pair_count_closed_form():
+    """Gen pairs = sum over gen frames t of F_g^2 (frames within w of t) + G * valid ref tokens."""
+    for geom in WINDOW_GEOMS:
+        fg, T, w = geom.gen_h * geom.gen_w, geom.gen_frames, geom.gen_window
+        F = geom.ref_h * geom.ref_w
+        nv = geom.ref_frames if geom.frame_valid is None else sum(geom.frame_valid)
+        want = sum(fg * fg * (min(T - 1, t + w) - max(0, t - w) + 1) for t in range(T)) + geom.n_gen * F * nv
+        assert oracle.pair_counts([geom], block_rows=7)[0] == want
