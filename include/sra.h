@@ -57,6 +57,7 @@ typedef struct sra_sample_geom {
   int32_t gen_frames, gen_h, gen_w;
   int32_t ref_frames, ref_h, ref_w;
   int32_t group_frames;              /* >= 1: ref frames per ref self-attention group          */
+  int32_t gen_window;                /* with SRA_FLAG_GEN_WINDOW: >= 0, see below; else ignored */
   const uint8_t* ref_frame_valid;    /* host, ref_frames bytes (0 = invalid); NULL = all valid */
 } sra_sample_geom;
 
@@ -78,8 +79,13 @@ typedef struct sra_problem {
  *   forward writes o_gen and lse_gen only; q_ref, o_ref and lse_ref are not read or written
  *   and may be NULL. The backward is that of the gen rows alone (equivalently: do_ref = 0):
  *   it writes dq_gen, dk_gen, dv_gen, dk_ref and dv_ref; q_ref, o_ref, lse_ref, do_ref and
- *   dq_ref are not touched and may be NULL. Pair counts and schedules omit the ref queries. */
-enum { SRA_FLAG_GEN_QUERIES_ONLY = 1u };
+ *   dq_ref are not touched and may be NULL. Pair counts and schedules omit the ref queries.
+ * SRA_FLAG_GEN_WINDOW: temporal window on generation-to-generation attention, the sparse
+ *   temporal attention of the super-resolution refiner (§2.4, which restricts each frame's
+ *   receptive field to a local neighbourhood of frames and gives no width): a gen query in
+ *   gen latent frame t sees the gen keys of frames t' with |t - t'| <= gen_window of its
+ *   sample, and still every valid reference key. Reference queries are unchanged. */
+enum { SRA_FLAG_GEN_QUERIES_ONLY = 1u, SRA_FLAG_GEN_WINDOW = 2u };
 
 /* Which schedule an inspection hook looks at. */
 enum {

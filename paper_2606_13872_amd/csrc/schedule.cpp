@@ -35,6 +35,11 @@ std::vector<Run> valid_runs(const SampleLayout& s, int32_t lo, int32_t hi) {
   return runs;
 }
 
+// Gen frames [f0, f1) a gen frame t sees under the sample's temporal window.
+Run gen_window_frames(const SampleLayout& s, int32_t t) {
+  return {std::max<int32_t>(0, t - s.window), std::min<int32_t>(s.gen_frames, t + s.window + 1)};
+}
+
 bool mul_ok(int64_t a, int64_t b, int64_t lim) { return a >= 0 && b >= 0 && (b == 0 || a <= lim / b); }
 
 }  // namespace
@@ -48,7 +53,11 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
     return p->head_dim > 0 ? SRA_ERR_UNSUPPORTED : SRA_ERR_INVALID_ARGUMENT;
   }
   if (!p->samples) { *err = "samples is NULL"; return SRA_ERR_INVALID_ARGUMENT; }
-  if (p->flags & ~uint32_t(SRA_FLAG_GEN_QUERIES_ONLY)) { *err = "unknown flag bits"; return SRA_ERR_INVALID_ARGUMENT; }
+  if (p->flags & ~uint32_t(SRA_FLAG_GEN_QUERIES_ONLY | SRA_FLAG_GEN_WINDOW)) {
+    *err = "unknown flag bits";
+    return SRA_ERR_INVALID_ARGUMENT;
+  }
+  const bool windowed = (p->flags & SRA_FLAG_GEN_WINDOW) != 0;
   if (!(std::isfinite(p->softmax_scale))) { *err = "softmax_scale is not finite"; return SRA_ERR_INVALID_ARGUMENT; }
   const int64_t hd = int64_t(p->num_heads) * p->head_dim;
   Layout L;
@@ -78,12 +87,17 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
       return SRA_ERR_INVALID_ARGUMENT;
     }
     if (g.group_frames < 1) { *err = tag + "group_frames must be >= 1"; return SRA_ERR_INVALID_ARGUMENT; }
+    if (windowed && g.gen_window < 0) { *err = tag + "gen_window must be >= 0"; return SRA_ERR_INVALID_ARGUMENT; }
     if (!mul_ok(g.gen_frames, int64_t(g.gen_h) * g.gen_w, kRowLimit) ||
         !mul_ok(g.ref_frames, int64_t(g.ref_h) * g.ref_w, kRowLimit)) {
       *err = tag + "token count overflows int32";
       return SRA_ERR_INVALID_ARGUMENT;
     }
     s.G = int64_t(g.gen_frames) * g.gen_h * g.gen_w;
+    s.Fg = int64_t(g.gen_h) * g.gen_w;
+    s.gen_frames = g.gen_frames;
+    // a window reaching every frame is no window (same schedule as full attention)
+    s.window = (windowed && g.gen_window < g.gen_frames - 1) ? g.gen_window : -1;
     s.F = g.ref_frames > 0 ? int64_t(g.ref_h) * g.ref_w : 0;
     s.R = int64_t(g.ref_frames) * s.F;
     s.ref_frames = g.ref_frames;
@@ -108,7 +122,15 @@ void closed_form_pairs(const Layout& L, int64_t* gen_pairs, int64_t* ref_pairs) 
   int64_t gp = 0, rp = 0;
   for (const SampleLayout& s : L.samples) {
     int64_t valid_frames = std::accumulate(s.valid.begin(), s.valid.end(), int64_t(0));
-    gp += s.G * (s.G + valid_frames * s.F);
+    gp += s.G * valid_frames * s.F;
+    if (s.window < 0) {
+      gp += s.G * s.G;
+    } else {
+      for (int32_t t = 0; t < s.gen_frames; ++t) {
+        const Run w = gen_window_frames(s, t);
+        gp += s.Fg * s.Fg * (w.f1 - w.f0);
+      }
+    }
     for (int32_t g0 = 0; g0 < s.ref_frames; g0 += s.group) {
       int64_t n = 0;
       for (int32_t f = g0; f < std::min(s.ref_frames, g0 + s.group); ++f) n += s.valid[f];
@@ -181,13 +203,25 @@ void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
   s->spans.clear();
   for (int32_t b = 0; b < L.batch; ++b) {
     const SampleLayout& sm = L.samples[b];
-    // gen queries: gen keys + every valid ref run
-    TileClass c{0, sm.gen_off, sm.G, int32_t(s->spans.size()), 0, b, 0};
-    s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
-    for (const Run& r : valid_runs(sm, 0, sm.ref_frames))
-      s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
-    c.span_cnt = int32_t(s->spans.size()) - c.span_off;
-    classes.push_back(c);
+    // gen queries: gen keys (all, or the frames of the temporal window) + every valid ref run.
+    // With a window, query tiles are cut per gen frame so that a tile shares one key set.
+    const std::vector<Run> ref_runs = valid_runs(sm, 0, sm.ref_frames);
+    auto gen_class = [&](int64_t row0, int64_t rows, int64_t key0, int64_t keys) {
+      TileClass c{0, row0, rows, int32_t(s->spans.size()), 0, b, 0};
+      s->spans.push_back({0, int32_t(key0), int32_t(keys), 0});
+      for (const Run& r : ref_runs)
+        s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
+      c.span_cnt = int32_t(s->spans.size()) - c.span_off;
+      classes.push_back(c);
+    };
+    if (sm.window < 0) {
+      gen_class(sm.gen_off, sm.G, sm.gen_off, sm.G);
+    } else {
+      for (int32_t t = 0; t < sm.gen_frames; ++t) {
+        const Run w = gen_window_frames(sm, t);
+        gen_class(sm.gen_off + t * sm.Fg, sm.Fg, sm.gen_off + w.f0 * sm.Fg, (w.f1 - w.f0) * sm.Fg);
+      }
+    }
     if (L.gen_only) continue;
     // ref queries: per group, keys = valid runs of the group; query tiles per valid run
     for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
@@ -211,10 +245,21 @@ void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
   s->spans.clear();
   for (int32_t b = 0; b < L.batch; ++b) {
     const SampleLayout& sm = L.samples[b];
-    // gen keys are seen by the gen queries of the sample only
-    int32_t gq = int32_t(s->spans.size());
-    s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
-    classes.push_back({0, sm.gen_off, sm.G, gq, 1, b, 0});
+    // gen keys are seen by the gen queries of the sample only (those of the frames within the
+    // temporal window, if any: the window is symmetric, so key frame t' is seen from the same
+    // frames that t' would see)
+    if (sm.window < 0) {
+      int32_t gq = int32_t(s->spans.size());
+      s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
+      classes.push_back({0, sm.gen_off, sm.G, gq, 1, b, 0});
+    } else {
+      for (int32_t t = 0; t < sm.gen_frames; ++t) {
+        const Run w = gen_window_frames(sm, t);
+        int32_t gq = int32_t(s->spans.size());
+        s->spans.push_back({0, int32_t(sm.gen_off + w.f0 * sm.Fg), int32_t((w.f1 - w.f0) * sm.Fg), 0});
+        classes.push_back({0, sm.gen_off + t * sm.Fg, sm.Fg, gq, 1, b, 0});
+      }
+    }
     // ref keys of a valid frame: gen queries + ref queries of the valid frames of its group
     for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
       std::vector<Run> runs = valid_runs(sm, g0, std::min(sm.ref_frames, g0 + sm.group));
@@ -270,7 +315,7 @@ std::string layout_key(const Layout& L) {
   auto put = [&k](int64_t v) { k.append(reinterpret_cast<const char*>(&v), sizeof v); };
   put(L.batch); put(L.heads); put(L.head_dim); put(L.gen_only ? 1 : 0);
   for (const SampleLayout& s : L.samples) {
-    put(s.G); put(s.R); put(s.F); put(s.ref_frames); put(s.group);
+    put(s.G); put(s.R); put(s.F); put(s.Fg); put(s.ref_frames); put(s.group); put(s.window);
     k.append(reinterpret_cast<const char*>(s.valid.data()), s.valid.size());
   }
   return k;

@@ -14,8 +14,10 @@ namespace sra {
 // Derived geometry of one sample.
 struct SampleLayout {
   int64_t G = 0, R = 0, F = 0;        // gen tokens, ref tokens, tokens per ref frame
+  int64_t Fg = 0;                     // tokens per gen frame
   int64_t gen_off = 0, ref_off = 0;   // first packed row of the sample in each stream
-  int32_t ref_frames = 0, group = 1;
+  int32_t gen_frames = 0, ref_frames = 0, group = 1;
+  int32_t window = -1;                // gen-gen temporal window in frames; -1 = none
   std::vector<uint8_t> valid;         // per ref frame, 0/1
 };
 

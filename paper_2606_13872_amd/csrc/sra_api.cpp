@@ -546,6 +546,6 @@ const char* sra_status_string(sra_status s) {
 
 const char* sra_last_error(void) { return g_last_error.c_str(); }
 
-int32_t sra_version(void) { return 100; }
+int32_t sra_version(void) { return 200; }
 
 }  // extern "C"

@@ -38,7 +38,7 @@ class _SampleGeom(ctypes.Structure):
     _fields_ = [
         ("gen_frames", ctypes.c_int32), ("gen_h", ctypes.c_int32), ("gen_w", ctypes.c_int32),
         ("ref_frames", ctypes.c_int32), ("ref_h", ctypes.c_int32), ("ref_w", ctypes.c_int32),
-        ("group_frames", ctypes.c_int32), ("ref_frame_valid", ctypes.c_void_p),
+        ("group_frames", ctypes.c_int32), ("gen_window", ctypes.c_int32), ("ref_frame_valid", ctypes.c_void_p),
     ]
 
 
@@ -98,6 +98,7 @@ def status_string(status: int) -> str:
 
 
 FLAG_GEN_QUERIES_ONLY = 1  # SRA_FLAG_GEN_QUERIES_ONLY: reference tokens are context only
+FLAG_GEN_WINDOW = 2        # SRA_FLAG_GEN_WINDOW: temporal window on gen-gen attention
 
 
 def _check(status: int) -> None:
@@ -119,6 +120,9 @@ class Problem:
         self.samples = list(samples)
         self._geoms = (_SampleGeom * max(1, len(self.samples)))()
         self._valid = []
+        # a window on any sample sets the flag; samples without one get a window over all frames
+        if any(getattr(g, "gen_window", None) is not None for g in self.samples):
+            flags |= FLAG_GEN_WINDOW
         for i, g in enumerate(self.samples):
             v = getattr(g, "frame_valid", None)
             ptr = None
@@ -126,8 +130,9 @@ class Problem:
                 buf = (ctypes.c_uint8 * max(1, len(v)))(*[1 if x else 0 for x in v])
                 self._valid.append(buf)
                 ptr = ctypes.cast(buf, ctypes.c_void_p)
+            w = getattr(g, "gen_window", None)
             self._geoms[i] = _SampleGeom(g.gen_frames, g.gen_h, g.gen_w, g.ref_frames, g.ref_h, g.ref_w,
-                                         getattr(g, "group_frames", 1), ptr)
+                                         getattr(g, "group_frames", 1), g.gen_frames if w is None else int(w), ptr)
         self.c = _Problem(len(self.samples), heads, head_dim, 0.0 if scale is None else float(scale),
                           ctypes.cast(self._geoms, ctypes.POINTER(_SampleGeom)),
                           gen_token_stride, ref_token_stride, flags)

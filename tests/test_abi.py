@@ -20,7 +20,7 @@ def test_library_exports_every_declared_function():
     L = sra.lib()
     for n in names:
         assert hasattr(L, n), n
-    assert L.sra_version() >= 100
+    assert L.sra_version() >= 200
     assert sra.status_string(0) == "SRA_OK"
     assert sra.status_string(3) == "SRA_ERR_WORKSPACE_TOO_SMALL"
 
@@ -49,7 +49,7 @@ def test_invalid_problems_are_rejected(samples, heads, d, stride, status):
 
 
 def test_flags_and_batch_validation():
-    for bad in (2, 4, 0x80000000, 3):
+    for bad in (4, 8, 0x80000000, 7):
         p = sra.Problem(GOOD, 1, 64, flags=bad)
         with pytest.raises(sra.SRAError) as e:
             p.workspace_size(False)
@@ -103,3 +103,16 @@ def test_flag_constant_matches_the_header():
     text = open(sra.HEADER_PATH).read()
     m = re.search(r"SRA_FLAG_GEN_QUERIES_ONLY\s*=\s*(\d+)u", text)
     assert m and int(m.group(1)) == sra.FLAG_GEN_QUERIES_ONLY
+
+
+def test_window_flag_constant_and_struct_layout():
+    import re
+    text = open(sra.HEADER_PATH).read()
+    m = re.search(r"SRA_FLAG_GEN_WINDOW\s*=\s*(\d+)u", text)
+    assert m and int(m.group(1)) == sra.FLAG_GEN_WINDOW
+    # gen_window fills the padding before the pointer: the struct keeps its size
+    assert ctypes.sizeof(sra._SampleGeom) == 40 and sra._SampleGeom.ref_frame_valid.offset == 32
+    bad = SampleGeom(3, 2, 2, 1, 2, 2, gen_window=-1)
+    with pytest.raises(sra.SRAError) as e:
+        sra.Problem([bad], 1, 64).workspace_size(False)
+    assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT

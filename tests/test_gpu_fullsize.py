@@ -88,7 +88,7 @@ def _close(name, got, want):
     assert rel <= REL, f"{name}: relative err {rel:.3e}"
 
 
-@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "varlen"])
+@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "varlen", "varlen_window"])
 def test_fullsize_forward_sampled_rows(name):
     w = workload(name)
     x = _inputs(w, grads=False)
@@ -129,7 +129,7 @@ def test_fullsize_dq_sampled_rows(name):
         _close(f"{name} dQ b{b}", got, want)
 
 
-@pytest.mark.parametrize("name", ["720p", "varlen"])
+@pytest.mark.parametrize("name", ["720p", "varlen", "varlen_window"])
 def test_fullsize_zero_keys_count_law(name):
     """K = 0 makes every visible logit 0, so LSE = ln(number of visible keys) for every row."""
     w = workload(name)
@@ -141,8 +141,12 @@ def test_fullsize_zero_keys_count_law(name):
     go, ro = _offsets(w.samples)
     for b, geom in enumerate(w.samples):
         F = geom.ref_h * geom.ref_w
-        lg = l_gen[:, go[b]:go[b + 1]]
-        assert torch.all((lg.double() - math.log(geom.n_gen + geom.n_ref)).abs() < 1e-5), f"gen rows, sample {b}"
+        lg = l_gen[:, go[b]:go[b + 1]].double()
+        fg, T, w = geom.gen_h * geom.gen_w, geom.gen_frames, geom.gen_window
+        for t in range(T):
+            seen = T if w is None else min(T - 1, t + w) - max(0, t - w) + 1
+            cnt = seen * fg + geom.n_ref
+            assert torch.all((lg[:, t * fg:(t + 1) * fg] - math.log(cnt)).abs() < 1e-5), f"gen frame {t}, sample {b}"
         if geom.n_ref:
             lr = l_ref[:, ro[b]:ro[b + 1]]
             assert torch.all((lr.double() - math.log(F * geom.group_frames)).abs() < 1e-5), f"ref rows, sample {b}"

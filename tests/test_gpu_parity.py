@@ -98,6 +98,12 @@ CASES = {
                 SampleGeom(2, 8, 8, 3, 8, 8, group_frames=3, frame_valid=[1, 1, 0])], 2, 128, 18, True),
     "d64_multi_tile": ([SampleGeom(2, 18, 18, 3, 12, 12)], 2, 64, 19, False),
     "d64_invalid_groups": ([SampleGeom(1, 9, 9, 5, 7, 5, group_frames=2, frame_valid=[1, 1, 0, 1, 1])], 2, 64, 20, True),
+    # the refiner's temporal window on gen-gen attention (frames of 300 / 143 / 70 tokens)
+    "window": ([SampleGeom(5, 15, 20, 3, 10, 13, gen_window=1)], 2, 128, 26, True),
+    "window_varlen": ([SampleGeom(4, 11, 13, 2, 7, 9, frame_valid=[1, 0], gen_window=0),
+                       SampleGeom(3, 10, 7, 3, 5, 6, group_frames=2, gen_window=1),
+                       SampleGeom(2, 9, 9, 2, 9, 9)], 2, 128, 27, False),
+    "d64_window": ([SampleGeom(6, 9, 9, 2, 9, 9, gen_window=2)], 2, 64, 28, False),
 }
 
 

@@ -29,6 +29,10 @@ GEOMS = [
     [SampleGeom(2, 10, 13, 3, 10, 13), SampleGeom(1, 17, 3, 2, 7, 7),      # varlen batch
      SampleGeom(3, 5, 5, 0, 5, 5), SampleGeom(1, 20, 20, 4, 6, 6, group_frames=2, frame_valid=[1, 1, 0, 1])],
     [SampleGeom(1, 16, 16, 2, 16, 16, group_frames=1)],                    # tile-aligned sizes
+    [SampleGeom(5, 9, 13, 3, 6, 9, gen_window=1)],                         # temporal window
+    [SampleGeom(6, 7, 7, 4, 5, 5, group_frames=2, frame_valid=[1, 0, 1, 1], gen_window=0),
+     SampleGeom(4, 20, 15, 2, 9, 9, gen_window=2), SampleGeom(3, 6, 6, 1, 6, 6)],
+    [SampleGeom(3, 10, 10, 2, 4, 4, gen_window=5)],                        # window >= all frames
 ]
 
 
