@@ -46,6 +46,8 @@ def _args():
     ap.add_argument("--workload", default="720p", help="720p (default) or varlen")
     ap.add_argument("--sweep-reps", type=int, default=2, help="forward calls per sweep point (0 = skip)")
     ap.add_argument("--cpu-rows", type=int, default=3072, help="gen rows in the CPU-oracle sample (0 = skip)")
+    ap.add_argument("--gen-only-reps", type=int, default=None,
+                    help="forward calls timed with the reference as context only (default: --steps; 0 = skip)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="run one plain copy kernel (torch.neg, fp32) over this many MiB first: the "
                          "calibration for the HBM byte counters")
@@ -220,6 +222,24 @@ def _cpu_baseline(x_gpu, w, gen_rows, torch):
     }
 
 
+def _gen_only(sra, torch, ins, fo, w, H, d, reps, line):
+    """Forward with the reference as cached context only (gen rows alone), timed."""
+    go_out = {"o_gen": fo["o_gen"], "lse_gen": fo["lse_gen"], "workspace": fo["workspace"]}
+    sra.forward(ins[0], ins[1], ins[2], None, ins[4], ins[5], w.samples, out=go_out, gen_queries_only=True)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        sra.forward(ins[0], ins[1], ins[2], None, ins[4], ins[5], w.samples, out=go_out, gen_queries_only=True)
+    e1.record()
+    torch.cuda.synchronize()
+    go_ms = e0.elapsed_time(e1) / reps
+    go_pairs, _ = sra.pair_counts(w.samples, H, d, flags=sra.FLAG_GEN_QUERIES_ONLY)
+    line["gen_queries_only_fwd"] = {"ms": round(go_ms, 3),
+                                    "tflops": round(4 * d * go_pairs * H / (go_ms * 1e-3) / 1e12, 2)}
+    print(f"[bench] gen-only forward {go_ms:.2f} ms", file=sys.stderr, flush=True)
+
+
 def main():
     args = _args()
     if args.pmc_summary:
@@ -310,20 +330,9 @@ def main():
         "roofline": roofline,
     }
     # reference as cached context only (the denoising-step path): gen rows alone
-    go_out = {"o_gen": fo["o_gen"], "lse_gen": fo["lse_gen"], "workspace": fo["workspace"]}
-    sra.forward(ins[0], ins[1], ins[2], None, ins[4], ins[5], w.samples, out=go_out, gen_queries_only=True)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        sra.forward(ins[0], ins[1], ins[2], None, ins[4], ins[5], w.samples, out=go_out, gen_queries_only=True)
-    e1.record()
-    torch.cuda.synchronize()
-    go_ms = e0.elapsed_time(e1) / args.steps
-    go_pairs, _ = sra.pair_counts(w.samples, H, d, flags=sra.FLAG_GEN_QUERIES_ONLY)
-    line["gen_queries_only_fwd"] = {"ms": round(go_ms, 3),
-                                    "tflops": round(4 * d * go_pairs * H / (go_ms * 1e-3) / 1e12, 2)}
-    print(f"[bench] gen-only forward {go_ms:.2f} ms", file=sys.stderr, flush=True)
+    go_reps = args.steps if args.gen_only_reps is None else args.gen_only_reps
+    if go_reps > 0:
+        _gen_only(sra, torch, ins, fo, w, H, d, go_reps, line)
     if args.cpu_rows > 0:
         print("[bench] cpu oracle sample", file=sys.stderr, flush=True)
         line["cpu_baseline"] = _cpu_baseline(x, w, args.cpu_rows, torch)

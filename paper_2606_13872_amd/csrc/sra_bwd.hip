@@ -77,9 +77,9 @@ struct DqState {
 
 // One 32-key step of dQ for the wave's 32 query rows (S^T, dP^T with lanes = queries).
 template <int D, bool kMask>
-__device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const __bf16* ktt, const __bf16* vt,
-                                        int nvalid, float sl2) {
-  constexpr int NC = D / 16, ND = D / 32, RK = kRowPadRS<D>, RKT = kTrPadRS<D>, RV = kRowPadRS<D>;
+__device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const __bf16* vt, int nvalid,
+                                        float sl2) {
+  constexpr int NC = D / 16, ND = D / 32, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
   floatx16 s = floatx16{}, dp = floatx16{};
 #pragma unroll
@@ -104,8 +104,8 @@ __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const 
     const int r0 = 16 * c2 + trow;
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
-      const bf16x8 kta = cat8(lds_read_tr(ktt + r0 * RKT + db * 32 + tcol),
-                              lds_read_tr(ktt + (r0 + 8) * RKT + db * 32 + tcol));
+      const bf16x8 kta = cat8(lds_read_tr(kt + r0 * RK + db * 32 + tcol),
+                              lds_read_tr(kt + (r0 + 8) * RK + db * 32 + tcol));
       st.dq[db] = mfma32(kta, dsf, st.dq[db]);
     }
   }
@@ -114,11 +114,10 @@ __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const 
 template <int D>
 __global__ void __launch_bounds__(kDqWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dq_kernel(BwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RK = kRowPadRS<D>, RKT = kTrPadRS<D>,
-                RV = kRowPadRS<D>;
-  // K is staged twice: at the row-fragment stride and at the transpose-read stride
+  constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
+  // K is read both as row fragments and through the transpose read: one copy at the stride
+  // that serves both (a second copy at the transpose stride measured slower)
   __shared__ __attribute__((aligned(1024))) __bf16 ks[2][PaddedTile<D, BK, RK>::kElems];
-  __shared__ __attribute__((aligned(1024))) __bf16 kts[2][PaddedTile<D, BK, RKT>::kElems];
   __shared__ __attribute__((aligned(1024))) __bf16 vs[2][PaddedTile<D, BK, RV>::kElems];
 
   const WorkItem it = a.items[blockIdx.x];
@@ -153,12 +152,10 @@ sra_dq_kernel(BwdArgs a) {
   SpanCursor ld;
   ld.init(sp, it.span_cnt);
   TileLoader<D, BK, RK, kDqWaves> kl[2];
-  TileLoader<D, BK, RKT, kDqWaves> ktl[2];
   TileLoader<D, BK, RV, kDqWaves> vl[2];
 #pragma unroll
   for (int ss = 0; ss < 2; ++ss) {
     kl[ss].init(a.in_stride[ss], h, wave);
-    ktl[ss].init(a.in_stride[ss], h, wave);
     vl[ss].init(a.in_stride[ss], h, wave);
   }
   auto issue = [&](int b) {
@@ -167,16 +164,13 @@ sra_dq_kernel(BwdArgs a) {
       const int64_t row0 = int64_t(ld.start() + ld.off) * a.in_stride[ss];
       if (ss == 0) {
         kl[0].issue(ks[b], a.k[0] + row0, wave);
-        ktl[0].issue(kts[b], a.k[0] + row0, wave);
         vl[0].issue(vs[b], a.v[0] + row0, wave);
       } else {
         kl[1].issue(ks[b], a.k[1] + row0, wave);
-        ktl[1].issue(kts[b], a.k[1] + row0, wave);
         vl[1].issue(vs[b], a.v[1] + row0, wave);
       }
     } else {
       tile_load_lds<D, BK, RK, kDqWaves>(ks[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
-      tile_load_lds<D, BK, RKT, kDqWaves>(kts[b], a.k[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
       tile_load_lds<D, BK, RV, kDqWaves>(vs[b], a.v[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
     }
     ld.advance(BK);
@@ -191,13 +185,13 @@ sra_dq_kernel(BwdArgs a) {
     const int full = len / BK;
     for (int j = 0; j < full; ++j, ++t) {
       if (t + 1 < T) issue((t + 1) & 1);
-      if (active) dq_step<D, false>(st, ks[t & 1], kts[t & 1], vs[t & 1], BK, sl2);
+      if (active) dq_step<D, false>(st, ks[t & 1], vs[t & 1], BK, sl2);
       wait_vmem();
       __syncthreads();
     }
     if (len % BK) {
       if (t + 1 < T) issue((t + 1) & 1);
-      if (active) dq_step<D, true>(st, ks[t & 1], kts[t & 1], vs[t & 1], len % BK, sl2);
+      if (active) dq_step<D, true>(st, ks[t & 1], vs[t & 1], len % BK, sl2);
       wait_vmem();
       __syncthreads();
       ++t;
