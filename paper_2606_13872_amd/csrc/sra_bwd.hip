@@ -65,6 +65,7 @@ hipError_t launch_delta(const DeltaArgs& a, int head_dim, hipStream_t stream) {
 // --------------------------------------------------------------------------- dq
 namespace {
 constexpr int kDqWaves = kDqQueryTile / 32;
+constexpr int kDqBufs = 4;
 }
 
 template <int D>
@@ -116,9 +117,12 @@ __global__ void __launch_bounds__(kDqWaves * 64) __attribute__((amdgpu_waves_per
 sra_dq_kernel(BwdArgs a) {
   constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
   // K is read both as row fragments and through the transpose read: one copy at the stride
-  // that serves both (a second copy at the transpose stride measured slower)
-  __shared__ __attribute__((aligned(1024))) __bf16 ks[2][PaddedTile<D, BK, RK>::kElems];
-  __shared__ __attribute__((aligned(1024))) __bf16 vs[2][PaddedTile<D, BK, RV>::kElems];
+  // that serves both (a second copy at the transpose stride measured slower). Key tiles
+  // rotate through kDqBufs buffers, are loaded two steps ahead, and the workgroup meets at a
+  // barrier after every second step (as in the dK/dV kernel).
+  constexpr int NB = kDqBufs;
+  __shared__ __attribute__((aligned(1024))) __bf16 ks[NB][PaddedTile<D, BK, RK>::kElems];
+  __shared__ __attribute__((aligned(1024))) __bf16 vs[NB][PaddedTile<D, BK, RV>::kElems];
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
@@ -177,23 +181,31 @@ sra_dq_kernel(BwdArgs a) {
   };
 
   issue(0);
+  if (T > 1) issue(1);
   wait_vmem();
   __syncthreads();
+  // Step t reads buffer t % NB and loads step t + 2 into buffer (t + 2) % NB. That buffer's
+  // last reader, step t - 2, finished before the barrier ending step t - 2 or t - 1
+  // (whichever is odd); the tiles of step t landed before that same barrier.
   int t = 0;
   for (int si = 0; si < it.span_cnt; ++si) {
     const int len = __builtin_amdgcn_readfirstlane(sp[si].len);
     const int full = len / BK;
     for (int j = 0; j < full; ++j, ++t) {
-      if (t + 1 < T) issue((t + 1) & 1);
-      if (active) dq_step<D, false>(st, ks[t & 1], vs[t & 1], BK, sl2);
-      wait_vmem();
-      __syncthreads();
+      if (t + 2 < T) issue((t + 2) % NB);
+      if (active) dq_step<D, false>(st, ks[t % NB], vs[t % NB], BK, sl2);
+      if (t & 1) {
+        wait_vmem();
+        __syncthreads();
+      }
     }
     if (len % BK) {
-      if (t + 1 < T) issue((t + 1) & 1);
-      if (active) dq_step<D, true>(st, ks[t & 1], vs[t & 1], len % BK, sl2);
-      wait_vmem();
-      __syncthreads();
+      if (t + 2 < T) issue((t + 2) % NB);
+      if (active) dq_step<D, true>(st, ks[t % NB], vs[t % NB], len % BK, sl2);
+      if (t & 1) {
+        wait_vmem();
+        __syncthreads();
+      }
       ++t;
     }
   }
