@@ -116,8 +116,8 @@ template <int D>
 __global__ void __launch_bounds__(kDqWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dq_kernel(BwdArgs a) {
   constexpr int NC = D / 16, ND = D / 32, BK = kDqKeyStep, RK = kBothPadRS<D>, RV = kRowPadRS<D>;
-  // K is read both as row fragments and through the transpose read: one copy at the stride
-  // that serves both (a second copy at the transpose stride measured slower). Key tiles
+  // K is read both as row fragments and through the transpose read, from one copy at D + 24
+  // (measured faster here than the permuted-row layout or a second copy). Key tiles
   // rotate through kDqBufs buffers, are loaded two steps ahead, and the workgroup meets at a
   // barrier after every second step (as in the dK/dV kernel).
   constexpr int NB = kDqBufs;
@@ -251,8 +251,9 @@ template <int D, bool kMask>
 __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, const __bf16* qt,
                                          const __bf16* dt, const float* lse_s, const float* ndlt_s,
                                          int nvalid, float sl2) {
-  constexpr int NC = D / 16, ND = D / 32, RQ = kBothPadRS<D>;
+  constexpr int NC = D / 16, ND = D / 32, RQ = kRowPadRS<D>;  // Q and dO rows permuted
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
+  const int qrow = perm16(l32);
   // dP starts from -D (staged negated in LDS, read in the accumulator's row order), so the
   // MFMAs leave dP - D and dS = P * (dP - D) is one multiply
   floatx16 s = floatx16{}, dp;
@@ -264,9 +265,9 @@ __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, co
   }
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
-    const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qt + l32 * RQ + c * 16 + half * 8);
+    const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qt + qrow * RQ + c * 16 + half * 8);
     const bf16x8 kb = *reinterpret_cast<const bf16x8*>(krow + c * 16);
-    const bf16x8 da = *reinterpret_cast<const bf16x8*>(dt + l32 * RQ + c * 16 + half * 8);
+    const bf16x8 da = *reinterpret_cast<const bf16x8*>(dt + qrow * RQ + c * 16 + half * 8);
     s = mfma32(qa, kb, s);
     dp = mfma32(da, st.vf[c], dp);
   }
@@ -283,21 +284,22 @@ __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, co
       dp[i] = p * dp[i];
     }
   }
-  // dV^T += dO^T P and dK^T += Q^T dS ; dO^T and Q^T fragments via the transpose read
+  // dV^T += dO^T P and dK^T += Q^T dS ; dO^T and Q^T fragments via the transpose read (rows
+  // r0 and r0 + 8 sit at physical rows perm16(r0) and perm16(r0) + 2)
   const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const int trow = 4 * half + ((lane & 15) >> 2);
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2) {
     const bf16x8 pb = to_bf16x8(s, 8 * c2);
     const bf16x8 sb = to_bf16x8(dp, 8 * c2);
-    const int r0 = 16 * c2 + trow;
+    const int r0 = 16 * c2 + perm16(trow);
 #pragma unroll
     for (int db = 0; db < ND; ++db) {
       const bf16x8 dta = cat8(lds_read_tr(dt + r0 * RQ + db * 32 + tcol),
-                              lds_read_tr(dt + (r0 + 8) * RQ + db * 32 + tcol));
+                              lds_read_tr(dt + (r0 + 2) * RQ + db * 32 + tcol));
       st.dv[db] = mfma32(dta, pb, st.dv[db]);
       const bf16x8 qta = cat8(lds_read_tr(qt + r0 * RQ + db * 32 + tcol),
-                              lds_read_tr(qt + (r0 + 8) * RQ + db * 32 + tcol));
+                              lds_read_tr(qt + (r0 + 2) * RQ + db * 32 + tcol));
       st.dk[db] = mfma32(qta, sb, st.dk[db]);
     }
   }
@@ -314,7 +316,7 @@ constexpr int kDkvBufs = 4;
 template <int D, bool kOneStride>
 __global__ void __launch_bounds__(kDkvWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_dkv_kernel(BwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BQ = kDkvQueryStep, RK = kRowPadRS<D>, RQ = kBothPadRS<D>;
+  constexpr int NC = D / 16, ND = D / 32, BQ = kDkvQueryStep, RK = kRowPadRS<D>, RQ = kRowPadRS<D>;
   constexpr int NB = kDkvBufs;
   using KT = PaddedTile<D, kDkvKeyTile, RK>;
   using QT = PaddedTile<D, BQ, RQ>;
@@ -357,7 +359,7 @@ sra_dkv_kernel(BwdArgs a) {
   SpanCursor ld;
   ld.init(sp, it.span_cnt);
   constexpr int NL = kOneStride ? 1 : 2;
-  TileLoader<D, BQ, RQ, kDkvWaves> ql[NL], dl;
+  TileLoader<D, BQ, RQ, kDkvWaves, true> ql[NL], dl;  // Q and dO rows permuted
 #pragma unroll
   for (int ss = 0; ss < NL; ++ss) ql[ss].init(a.in_stride[ss], h, wave);
   dl.init(dstride, h, wave);
@@ -374,8 +376,8 @@ sra_dkv_kernel(BwdArgs a) {
         ql[NL - 1].issue(qs[b], a.q[1] + row0 * a.in_stride[1], wave);
       dl.issue(dos[b], a.dout[ss] + row0 * dstride, wave);
     } else {
-      tile_load_lds<D, BQ, RQ, kDkvWaves>(qs[b], a.q[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
-      tile_load_lds<D, BQ, RQ, kDkvWaves>(dos[b], a.dout[ss], dstride, h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BQ, RQ, kDkvWaves, true>(qs[b], a.q[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
+      tile_load_lds<D, BQ, RQ, kDkvWaves, true>(dos[b], a.dout[ss], dstride, h, ld.start(), ld.len(), ld.off, wave);
     }
     if (wave == 0 && lane < BQ) {
       const int rr = ld.start() + min(ld.off + lane, ld.len() - 1);

@@ -51,10 +51,18 @@ __device__ __forceinline__ void tile_store(const TileRegs<D, NR>& t, __bf16* lds
 //   304 B  (D + 24)        128                           122
 //   320 B  (D + 32)         32                           203
 // so tiles read only as row fragments use D + 8, tiles read only through the transpose read
-// use D + 32, and tiles read both ways use D + 24.
+// use D + 32, and tiles read both ways use D + 24 or D + 8 with permuted rows (below).
 template <int D> constexpr int kRowPadRS = D + 8;
 template <int D> constexpr int kTrPadRS = D + 32;
 template <int D> constexpr int kBothPadRS = D + 24;
+// Tiles read both as row fragments and through the transpose read are stored at the
+// row-fragment stride (D + 8) with their rows permuted inside each block of 16: logical row
+// r = 4a + b (a, b < 4) sits at physical row 4b + a. A row fragment (16 consecutive rows, one
+// 16-byte chunk each) still meets 16 distinct bank groups, and so does a transpose read
+// (4 consecutive rows, 4 chunks each), which the plain D + 8 stride does not give. The map is
+// its own inverse, and for r < 8 it sends r + 8 to perm16(r) + 2.
+__host__ __device__ constexpr int perm16(int r) { return (r & ~15) | ((r & 3) << 2) | ((r >> 2) & 3); }
+
 template <int D, int NR, int RS>
 struct PaddedTile {
   static constexpr int kSlotsPerRow = RS / 8;                          // 16-byte slots per row
@@ -88,10 +96,11 @@ __device__ __forceinline__ void lds_dma_x4(const void* g, void* lds) {
 // (LDS base + 16 l), so lane l fetches the global chunk that belongs there; lanes that land on
 // a pad slot fetch an in-bounds chunk that nothing reads. Rows past the span end are clamped
 // to its last row (the kernels mask them). Instructions are dealt over the NW waves.
-template <int D, int NR, int RS, int NW>
+template <int D, int NR, int RS, int NW, bool kPerm = false>
 __device__ __forceinline__ void tile_load_lds(__bf16* lds, const __bf16* __restrict__ src, int64_t stride,
                                               int head, int start, int len, int off, int wave) {
   using TL = PaddedTile<D, NR, RS>;
+  static_assert(!kPerm || NR % 16 == 0, "permuted tiles hold whole 16-row blocks");
   constexpr int SPR = TL::kSlotsPerRow, CPR = D / 8;
   const int lane = threadIdx.x & 63;
 #pragma unroll
@@ -99,7 +108,8 @@ __device__ __forceinline__ void tile_load_lds(__bf16* lds, const __bf16* __restr
     const int ins = wave + j * NW;
     if (ins < TL::kInstr) {
       const int p = ins * 64 + lane;
-      const int row = min(p / SPR, NR - 1);
+      const int prow = min(p / SPR, NR - 1);
+      const int row = kPerm ? perm16(prow) : prow;  // logical row stored at physical row prow
       const int slot = p % SPR;
       const int ch = slot < CPR ? slot : 0;
       const int rr = min(off + row, len - 1);
@@ -111,9 +121,10 @@ __device__ __forceinline__ void tile_load_lds(__bf16* lds, const __bf16* __restr
 
 // Per-lane address offsets of the direct loads of a padded tile, for tiles whose NR rows all
 // lie inside the span (no clamping): lane offsets are fixed, only the tile's first row moves.
-template <int D, int NR, int RS, int NW>
+template <int D, int NR, int RS, int NW, bool kPerm = false>
 struct TileLoader {
   using TL = PaddedTile<D, NR, RS>;
+  static_assert(!kPerm || NR % 16 == 0, "permuted tiles hold whole 16-row blocks");
   static constexpr int kSlots = (TL::kInstr + NW - 1) / NW;
   int voff[kSlots];  // element offset of this lane's chunk from the tile's first row
   __device__ __forceinline__ void init(int64_t stride, int head, int wave) {
@@ -122,7 +133,8 @@ struct TileLoader {
 #pragma unroll
     for (int j = 0; j < kSlots; ++j) {
       const int p = (wave + j * NW) * 64 + lane;
-      const int row = min(p / SPR, NR - 1);
+      const int prow = min(p / SPR, NR - 1);
+      const int row = kPerm ? perm16(prow) : prow;
       const int slot = p % SPR;
       voff[j] = int(row * stride) + head * D + (slot < CPR ? slot : 0) * 8;
     }
