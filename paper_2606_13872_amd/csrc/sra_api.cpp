@@ -130,9 +130,10 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 
 size_t fwd_workspace(const CachedPlan& cp) { return cp.fwd.bytes; }
 size_t bwd_workspace(const CachedPlan& cp, const Layout& L) {
+  // schedule, then -D and the LSE in log2 units per query row of each stream
   size_t b = cp.bwd.bytes;
-  b += align_up(size_t(L.heads) * L.sum_gen * sizeof(float));
-  b += align_up(size_t(L.heads) * L.sum_ref * sizeof(float));
+  b += 2 * align_up(size_t(L.heads) * L.sum_gen * sizeof(float));
+  b += 2 * align_up(size_t(L.heads) * L.sum_ref * sizeof(float));
   return b;
 }
 
@@ -350,16 +351,24 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
   if (st != SRA_OK) return st;
   hipError_t e = hipMemcpyAsync(ws, src, cp->bwd.bytes, hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "schedule upload");
-  float* delta_gen = reinterpret_cast<float*>(ws + cp->bwd.bytes);
-  float* delta_ref = reinterpret_cast<float*>(ws + cp->bwd.bytes + align_up(size_t(L.heads) * L.sum_gen * sizeof(float)));
+  const size_t gen_stat = align_up(size_t(L.heads) * L.sum_gen * sizeof(float));
+  const size_t ref_stat = align_up(size_t(L.heads) * L.sum_ref * sizeof(float));
+  float* ndelta_gen = reinterpret_cast<float*>(ws + cp->bwd.bytes);
+  float* lse2_gen = reinterpret_cast<float*>(ws + cp->bwd.bytes + gen_stat);
+  float* ndelta_ref = reinterpret_cast<float*>(ws + cp->bwd.bytes + 2 * gen_stat);
+  float* lse2_ref = reinterpret_cast<float*>(ws + cp->bwd.bytes + 2 * gen_stat + ref_stat);
 
   DeltaArgs d{};
   d.o[0] = static_cast<const __bf16*>(o_gen);
   d.o[1] = static_cast<const __bf16*>(o_ref);
   d.dout[0] = static_cast<const __bf16*>(do_gen);
   d.dout[1] = static_cast<const __bf16*>(do_ref);
-  d.delta[0] = delta_gen;
-  d.delta[1] = delta_ref;
+  d.lse[0] = lse_gen;
+  d.lse[1] = lse_ref;
+  d.ndelta[0] = ndelta_gen;
+  d.ndelta[1] = ndelta_ref;
+  d.lse2[0] = lse2_gen;
+  d.lse2[1] = lse2_ref;
   d.rows[0] = int32_t(L.sum_gen);
   d.rows[1] = L.gen_only ? 0 : int32_t(L.sum_ref);  // no ref query rows when gen-only
   d.heads = L.heads;
@@ -378,10 +387,10 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
   a.in_stride[1] = L.ref_stride;
   a.dout[0] = static_cast<const __bf16*>(do_gen);
   a.dout[1] = static_cast<const __bf16*>(do_ref);
-  a.lse[0] = lse_gen;
-  a.lse[1] = lse_ref;
-  a.delta[0] = delta_gen;
-  a.delta[1] = delta_ref;
+  a.lse2[0] = lse2_gen;
+  a.lse2[1] = lse2_ref;
+  a.ndelta[0] = ndelta_gen;
+  a.ndelta[1] = ndelta_ref;
   a.dq[0] = static_cast<__bf16*>(dq_gen);
   a.dk[0] = static_cast<__bf16*>(dk_gen);
   a.dv[0] = static_cast<__bf16*>(dv_gen);

@@ -5,7 +5,8 @@
 // the visible keys, D = rowsum(dO * O),
 //     dV = P^T dO,   dP = dO V^T,   dS = P * (dP - D),   dQ = scale dS K,   dK = scale dS^T Q.
 // Three kernels, all deterministic (no atomics):
-//   delta : D for every query row (HBM bound).
+//   delta : -D and the log-sum-exp in log2 units for every query row (HBM bound); the other
+//           two kernels fetch both per row and use them without further arithmetic.
 //   dq    : query-major, like the forward: S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T.
 //   dkv   : key-major: each wave keeps 32 keys' K and V in VGPRs and streams the query rows
 //           that see those keys (gen keys: the gen queries of the sample; ref keys: the gen
@@ -44,7 +45,9 @@ __global__ void __launch_bounds__(kThreads) sra_delta_kernel(DeltaArgs a, int s)
   if (pair < total && sub == 0) {
     const int64_t row = pair / a.heads;
     const int h = int(pair % a.heads);
-    a.delta[s][int64_t(h) * a.rows[s] + row] = acc;
+    const int64_t i = int64_t(h) * a.rows[s] + row;
+    a.ndelta[s][i] = -acc;
+    a.lse2[s][i] = a.lse[s][i] * kLog2e;
   }
 }
 
@@ -73,7 +76,7 @@ struct DqState {
   bf16x8 qf[D / 16];    // Q^T B fragments (lane = query)
   bf16x8 df[D / 16];    // dO^T B fragments (lane = query)
   floatx16 dq[D / 32];  // dQ^T accumulators, 32 head dims each
-  float lse2, dlt;      // the row's log-sum-exp (log2 units) and rowsum(dO * O)
+  float lse2, ndlt;     // the row's log-sum-exp (log2 units) and -rowsum(dO * O)
 };
 
 // One 32-key step of dQ for the wave's 32 query rows (S^T, dP^T with lanes = queries).
@@ -94,7 +97,7 @@ __device__ __forceinline__ void dq_step(DqState<D>& st, const __bf16* kt, const 
   for (int i = 0; i < 16; ++i) {
     float p = fast_exp2(fmaf(s[i], sl2, -st.lse2));
     if constexpr (kMask) p = (8 * (i >> 2) + 4 * half + (i & 3)) < nvalid ? p : 0.f;
-    s[i] = p * (dp[i] - st.dlt);
+    s[i] = p * (dp[i] + st.ndlt);
   }
   // dQ^T += K^T dS^T ; K^T fragments through the transpose read
   const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -147,8 +150,8 @@ sra_dq_kernel(BwdArgs a) {
     }
 #pragma unroll
     for (int db = 0; db < ND; ++db) st.dq[db] = floatx16{};
-    st.lse2 = a.lse[s][int64_t(h) * a.rows[s] + rr] * kLog2e;
-    st.dlt = a.delta[s][int64_t(h) * a.rows[s] + rr];
+    st.lse2 = a.lse2[s][int64_t(h) * a.rows[s] + rr];
+    st.ndlt = a.ndelta[s][int64_t(h) * a.rows[s] + rr];
   }
 
   const Span* sp = a.spans + it.span_off;
@@ -323,8 +326,8 @@ sra_dkv_kernel(BwdArgs a) {
   __shared__ __attribute__((aligned(1024))) __bf16 ktile[KT::kElems];
   __shared__ __attribute__((aligned(1024))) __bf16 qs[NB][QT::kElems];
   __shared__ __attribute__((aligned(1024))) __bf16 dos[NB][QT::kElems];
-  __shared__ __attribute__((aligned(16))) float lse_s[NB][BQ];
-  __shared__ __attribute__((aligned(16))) float ndlt_s[NB][BQ];  // -D
+  // per query row of a step: LSE (log2 units) in [0, BQ), -D in [BQ, 2 BQ)
+  __shared__ __attribute__((aligned(16))) float rstat[NB][2 * BQ];
 
   const WorkItem it = a.items[blockIdx.x];
   if (it.stream < 0) return;
@@ -363,10 +366,10 @@ sra_dkv_kernel(BwdArgs a) {
 #pragma unroll
   for (int ss = 0; ss < NL; ++ss) ql[ss].init(a.in_stride[ss], h, wave);
   dl.init(dstride, h, wave);
-  // wave 0 lanes < BQ fetch one query row's LSE (log2 units) and delta per step: slot 0 for
-  // even steps, slot 1 for odd ones; they reach LDS at the next barrier
-  float lr[2] = {0.f, 0.f}, dr[2] = {0.f, 0.f};
-  auto issue = [&](int b, int slot) {  // the next step in the cursor -> buffer b
+  // wave 0 copies the step's row statistics straight into LDS: lanes < 32 the LSE, the
+  // others -D (one row each, clamped at the span end like the tiles)
+  static_assert(BQ == 32, "one dword per lane covers both statistics of 32 rows");
+  auto issue = [&](int b) {  // the next step in the cursor -> buffer b
     const int ss = ld.stream();
     if (ld.off + BQ <= ld.len()) {
       const int64_t row0 = int64_t(ld.start() + ld.off);
@@ -379,40 +382,27 @@ sra_dkv_kernel(BwdArgs a) {
       tile_load_lds<D, BQ, RQ, kDkvWaves, true>(qs[b], a.q[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
       tile_load_lds<D, BQ, RQ, kDkvWaves, true>(dos[b], a.dout[ss], dstride, h, ld.start(), ld.len(), ld.off, wave);
     }
-    if (wave == 0 && lane < BQ) {
-      const int rr = ld.start() + min(ld.off + lane, ld.len() - 1);
-      const float l = a.lse[ss][int64_t(h) * a.rows[ss] + rr] * kLog2e;
-      const float d = -a.delta[ss][int64_t(h) * a.rows[ss] + rr];  // staged negated
-      if (slot == 0) {
-        lr[0] = l;
-        dr[0] = d;
-      } else {
-        lr[1] = l;
-        dr[1] = d;
-      }
+    if (wave == 0) {
+      const int rr = ld.start() + min(ld.off + l32, ld.len() - 1);
+      // both bases as uniform values first: a per-lane select of the argument slots would
+      // become a vector load of the pointer and a wait on every load in flight
+      const uint64_t pl = uniform_u64(reinterpret_cast<uint64_t>(a.lse2[ss]));
+      const uint64_t pn = uniform_u64(reinterpret_cast<uint64_t>(a.ndelta[ss]));
+      const float* src = reinterpret_cast<const float*>(half ? pn : pl);
+      lds_dma_x1(src + int64_t(h) * a.rows[ss] + rr, rstat[b]);
     }
     ld.advance(BQ);
   };
-  auto stage = [&](int b, int slot) {
-    if (wave == 0 && lane < BQ) {
-      lse_s[b][lane] = slot == 0 ? lr[0] : lr[1];
-      ndlt_s[b][lane] = slot == 0 ? dr[0] : dr[1];
-    }
-  };
 
-  issue(0, 0);
-  if (T > 1) issue(1, 1);
+  issue(0);
+  if (T > 1) issue(1);
   wait_vmem();
-  stage(0, 0);
-  if (T > 1) stage(1, 1);
   __syncthreads();
   // step t reads buffer t % NB and loads step t + 2 into buffer (t + 2) % NB, whose last
   // reader (step t - 2) finished before the barrier that ended step t - 1 or t - 2.
   auto step_tail = [&](int t) {
     if (t & 1) {  // every odd step: land the loads of steps t + 1 and t + 2, then meet
       wait_vmem();
-      if (t + 1 < T) stage((t + 1) % NB, (t + 1) & 1);
-      if (t + 2 < T) stage((t + 2) % NB, t & 1);
       __syncthreads();
     }
   };
@@ -422,14 +412,14 @@ sra_dkv_kernel(BwdArgs a) {
     const int full = len / BQ;
     for (int j = 0; j < full; ++j, ++t) {
       const int b = t % NB;
-      if (t + 2 < T) issue((t + 2) % NB, t & 1);
-      if (active) dkv_step<D, false>(st, krow, qs[b], dos[b], lse_s[b], ndlt_s[b], BQ, sl2);
+      if (t + 2 < T) issue((t + 2) % NB);
+      if (active) dkv_step<D, false>(st, krow, qs[b], dos[b], rstat[b], rstat[b] + BQ, BQ, sl2);
       step_tail(t);
     }
     if (len % BQ) {
       const int b = t % NB;
-      if (t + 2 < T) issue((t + 2) % NB, t & 1);
-      if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], lse_s[b], ndlt_s[b], len % BQ, sl2);
+      if (t + 2 < T) issue((t + 2) % NB);
+      if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], rstat[b], rstat[b] + BQ, len % BQ, sl2);
       step_tail(t);
       ++t;
     }

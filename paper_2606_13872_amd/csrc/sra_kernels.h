@@ -29,9 +29,9 @@ struct BwdArgs {
   const __bf16* k[2];
   const __bf16* v[2];
   int64_t in_stride[2];
-  const __bf16* dout[2];  // dense
-  const float* lse[2];    // [heads, rows], natural log
-  const float* delta[2];  // [heads, rows], rowsum(dO * O)
+  const __bf16* dout[2];   // dense
+  const float* lse2[2];    // [heads, rows], log-sum-exp in log2 units (written by the delta kernel)
+  const float* ndelta[2];  // [heads, rows], -rowsum(dO * O)
   __bf16* dq[2];
   __bf16* dk[2];
   __bf16* dv[2];
@@ -44,7 +44,9 @@ struct BwdArgs {
 struct DeltaArgs {
   const __bf16* o[2];
   const __bf16* dout[2];
-  float* delta[2];
+  const float* lse[2];  // [heads, rows], natural log (the forward's output)
+  float* ndelta[2];     // [heads, rows] <- -rowsum(dO * O)
+  float* lse2[2];       // [heads, rows] <- lse * log2(e)
   int32_t rows[2];
   int32_t heads;
 };

@@ -91,6 +91,29 @@ __device__ __forceinline__ void lds_dma_x4(const void* g, void* lds) {
       : "memory");
 }
 
+// A wave-uniform 64-bit value held in scalar registers.
+__device__ __forceinline__ uint64_t uniform_u64(uint64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(x >> 32));
+  return (uint64_t(hi) << 32) | lo;
+}
+
+// One dword per lane: lane l's 4 bytes land at (LDS base + 4 l).
+__device__ __forceinline__ void lds_dma_x1(const void* g, void* lds) {
+  const uint32_t la = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dword %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(la)
+      : "memory");
+}
+
 // Direct global -> LDS copy (gfx950 GLOBAL_LOAD_LDS_DWORDX4) of rows [off, off + NR) of a span
 // into a padded tile. Each wave instruction fills 1 KB of LDS: lane l writes the 16 bytes at
 // (LDS base + 16 l), so lane l fetches the global chunk that belongs there; lanes that land on
