@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsra.so")
 
-SOURCES = ["schedule.cpp", "sra_api.cpp", "sra_fwd.hip", "sra_bwd.hip"]
+SOURCES = ["schedule.cpp", "sra_api.cpp", "sra_fwd.hip", "sra_bwd.hip", "sra_dkv.hip"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -27,6 +27,10 @@ COMMON = [
 # Device code only for gfx950. Packed-FP32 instructions are disabled in device code.
 HIP_FLAGS = ["-x", "hip", "--offload-arch=gfx950", "-Xclang", "-target-feature",
              "-Xclang", "-packed-fp32-ops", "-munsafe-fp-atomics"]
+# The dK/dV kernel selects its compiler-visible MFMAs in VGPR form: its AGPRs hold the dK/dV
+# sums (written by inline-assembly MFMAs), and S/dP must stay in VGPRs next to them.
+EXTRA_FLAGS = {"sra_dkv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+COMPILE_TIMEOUT_S = 900
 
 
 def hipcc() -> str:
@@ -40,11 +44,11 @@ def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
     path = os.path.join(CSRC, src)
     if src.endswith(".hip"):
-        cmd = [hipcc(), *HIP_FLAGS, *COMMON, "-c", path, "-o", obj]
+        cmd = [hipcc(), *HIP_FLAGS, *EXTRA_FLAGS.get(src, []), *COMMON, "-c", path, "-o", obj]
     else:  # host-only C++ (the scheduler includes no HIP header)
         cmd = [hipcc(), *COMMON, "-c", path, "-o", obj] if src == "sra_api.cpp" else \
               ["g++", *COMMON, "-c", path, "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    r = subprocess.run(cmd, capture_output=True, text=True, timeout=COMPILE_TIMEOUT_S)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     return obj
@@ -52,7 +56,7 @@ def _compile(src: str) -> str:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=4) as ex:
+    with cf.ThreadPoolExecutor(max_workers=5) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs]

@@ -23,6 +23,16 @@ __device__ __forceinline__ floatx16 mfma32(bf16x8 a, bf16x8 b, floatx16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// acc += A B with the accumulator pinned to AGPRs. For kernels whose accumulators fill the
+// AGPR file for their whole run while the VGPRs hold the other MFMA operands and results; the
+// compiler sees no MFMA here, so the two wait states cover a VALU write of A or B just
+// before, and readers of acc must wait out the MFMA latency themselves.
+__device__ __forceinline__ void mfma32_agpr(floatx16& acc, bf16x8 a, bf16x8 b) {
+  asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+__device__ __forceinline__ bf16x8 ld8(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Combine a value held by lanes l and l^32 (the two halves of one MFMA output column).

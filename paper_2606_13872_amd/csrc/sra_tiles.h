@@ -114,6 +114,26 @@ __device__ __forceinline__ void lds_dma_x1(const void* g, void* lds) {
       : "memory");
 }
 
+// LDS byte address of a __shared__ object.
+template <class T>
+__device__ __forceinline__ uint32_t lds_addr(const T* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// lds_dma_x4 to an LDS byte address (uniform) computed by the caller.
+__device__ __forceinline__ void lds_dma_x4_at(const void* g, uint32_t la) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(__builtin_amdgcn_readfirstlane(la))
+      : "memory");
+}
+
 // Direct global -> LDS copy (gfx950 GLOBAL_LOAD_LDS_DWORDX4) of rows [off, off + NR) of a span
 // into a padded tile. Each wave instruction fills 1 KB of LDS: lane l writes the 16 bytes at
 // (LDS base + 16 l), so lane l fetches the global chunk that belongs there; lanes that land on
