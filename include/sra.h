@@ -10,9 +10,9 @@
  *     gen keys (§1, §8.2: the reference side attends only within itself). A group is `group_frames`
  *     consecutive reference latent frames; group_frames = 1 keeps the cost linear in the
  *     reference length (§1, §2.1);
- *   - tokens of invalid reference frames (§4.3, e.g. frames where the face is not visible)
- *     are neither keys nor queries: their outputs are 0, their log-sum-exp is -inf and
- *     their gradients are 0.
+ *   - tokens of invalid reference frames (§4.3, e.g. frames where the face is not visible),
+ *     and single reference tokens marked invalid, are neither keys nor queries: their
+ *     outputs are 0, their log-sum-exp is -inf and their gradients are 0.
  * Samples of a packed (varlen) batch never see each other.
  *
  * Conventions shared by every entry point
@@ -59,6 +59,11 @@ typedef struct sra_sample_geom {
   int32_t group_frames;              /* >= 1: ref frames per ref self-attention group          */
   int32_t gen_window;                /* with SRA_FLAG_GEN_WINDOW: >= 0, see below; else ignored */
   const uint8_t* ref_frame_valid;    /* host, ref_frames bytes (0 = invalid); NULL = all valid */
+  const uint8_t* ref_token_valid;    /* host, R bytes, frame-major (0 = invalid token); NULL =
+                                        every token of a valid frame. A ref token takes part iff
+                                        its frame and its own entry are valid (§4.3 invalid
+                                        tokens); invalid tokens are treated like tokens of
+                                        invalid frames. */
 } sra_sample_geom;
 
 typedef struct sra_problem {
@@ -132,8 +137,9 @@ sra_status sra_backward(const sra_problem* p,
 /* ---- host-only inspection hooks (no device needed; used to test the schedules) ---------- */
 
 /* Visible (query, key) pairs per head summed over samples, from the closed form
- * G*(G + R_valid) for gen queries and sum over groups of (valid tokens of the group)^2 for
- * ref queries. Either output pointer may be NULL. */
+ * G*(G + R_valid) for gen queries (G*R_valid plus the window's gen pairs with
+ * SRA_FLAG_GEN_WINDOW) and sum over groups of (valid tokens of the group)^2 for ref queries.
+ * Either output pointer may be NULL. */
 sra_status sra_pair_counts(const sra_problem* p, int64_t* gen_pairs, int64_t* ref_pairs);
 
 /* Sizes of schedule `which` (SRA_SCHED_*): work items (all heads) and span entries, and the

@@ -15,7 +15,8 @@ What it computes (Avatar V, §1 contributions; §2.1 "Sparse Reference Attention
     by default (group_frames = 1); see the module note below.
   * Invalid reference frames (§4.3: e.g. frames where the face is not visible) are
     removed as keys for every query and as queries (output 0, log-sum-exp -inf,
-    no gradient).
+    no gradient). §4.3 speaks of invalid tokens: a per-token mask of the reference
+    tokens (optional, ANDed with the frame mask) removes single tokens the same way.
 
 The oracle is the plain definition: an explicit boolean visibility mask M over the
 concatenated token order [gen ; ref] of one sample, logits S = scale * Q K^T, S = -inf
@@ -59,6 +60,20 @@ def frame_valid(geom) -> np.ndarray:
     return v
 
 
+def token_valid(geom) -> np.ndarray:
+    """Per-reference-token validity (§4.3 invalid tokens): the token's frame is valid and, when
+    the sample carries a token mask (ref_token_valid, one entry per reference token in packed
+    frame-major order), its own entry is nonzero."""
+    G, R, F = sample_sizes(geom)
+    v = np.repeat(frame_valid(geom), F) if R > 0 else np.zeros(0, dtype=bool)
+    t = getattr(geom, "ref_token_valid", None)
+    if t is not None:
+        t = np.asarray(t).astype(bool)
+        assert t.shape == (R,)
+        v = v & t
+    return v
+
+
 def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
     """Explicit visibility mask of one sample, rows and columns in [gen ; ref] order.
 
@@ -67,13 +82,15 @@ def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
                      |gframe(q) - gframe(k)| <= w when the sample has gen_window = w
                      (§2.4: the refiner's sparse temporal attention keeps each frame's
                      receptive field to a local neighbourhood of latent frames)
-      gen q, ref k : valid(frame(k))                    (§1: gen sees every reference token)
+      gen q, ref k : valid(k)                           (§1: gen sees every reference token)
       ref q, gen k : False                              (§1, §8.2: reference attends only within itself)
-      ref q, ref k : valid(frame(q)) and valid(frame(k)) and group(q) == group(k)
+      ref q, ref k : valid(q) and valid(k) and group(q) == group(k)
+    where valid(t) is the token validity of token_valid (its frame's, and its own entry of
+    the token mask when there is one).
     `rows` selects a subset of query rows (row-block mode for large shapes).
     """
     G, R, F = sample_sizes(geom)
-    v = frame_valid(geom)
+    tv = token_valid(geom)
     g = int(geom.group_frames)
     assert g >= 1
     if rows is None:
@@ -82,7 +99,7 @@ def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
     M = np.zeros((rows.size, G + R), dtype=bool)
     is_gen = rows < G
     key_frame = np.arange(R) // F if F > 0 else np.zeros(0, dtype=np.int64)
-    key_valid = v[key_frame] if R > 0 else np.zeros(0, dtype=bool)
+    key_valid = tv
     key_group = key_frame // g
     # generation query rows
     w = getattr(geom, "gen_window", None)
@@ -100,7 +117,7 @@ def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
     if ref_rows.size:
         j = rows[ref_rows] - G
         q_frame = j // F
-        q_valid = v[q_frame]
+        q_valid = tv[j]
         q_group = q_frame // g
         blk = q_valid[:, None] & key_valid[None, :] & (q_group[:, None] == key_group[None, :])
         M[np.ix_(ref_rows, np.arange(G, G + R))] = blk

@@ -1,10 +1,12 @@
 // Geometry -> visibility runs -> tile schedules (host).
 //
 // Visibility (Avatar V §1, §2.1, §4.3, §8): a gen query sees every gen key of its sample and
-// every key of a valid ref frame of its sample; a ref query of a valid frame sees the keys
-// of the valid frames of its own group of `group_frames` frames. The rule is expressed
-// here as contiguous row ranges ("spans"), so each work item's kernel loop visits only
-// visible key (or query) rows and masks nothing but the ragged end of a span.
+// every valid ref key of its sample; a valid ref query sees the valid ref keys of its own
+// group of `group_frames` frames. A ref token is valid when its frame is and, if the sample
+// carries a token mask, its own entry is (§4.3 invalid tokens). The rule is expressed here
+// as contiguous row ranges ("spans") built from the runs of valid ref rows, so each work
+// item's kernel loop visits only visible key (or query) rows and masks nothing but the
+// ragged end of a span.
 #include "schedule.hpp"
 
 #include <algorithm>
@@ -16,23 +18,27 @@ namespace sra {
 
 namespace {
 
-struct Run {  // [f0, f1) frames, all valid
+struct Run {  // [f0, f1) frames
   int32_t f0, f1;
 };
 
-// Maximal runs of valid frames inside [lo, hi).
-std::vector<Run> valid_runs(const SampleLayout& s, int32_t lo, int32_t hi) {
-  std::vector<Run> runs;
-  int32_t f = lo;
-  while (f < hi) {
-    while (f < hi && !s.valid[f]) ++f;
-    if (f >= hi) break;
-    int32_t g = f;
-    while (g < hi && s.valid[g]) ++g;
-    runs.push_back({f, g});
-    f = g;
+struct RowRun {  // [r0, r1) ref rows (sample-relative), all valid
+  int64_t r0, r1;
+};
+
+// Maximal runs of valid ref rows inside [lo, hi).
+std::vector<RowRun> valid_runs(const SampleLayout& s, int64_t lo, int64_t hi) {
+  std::vector<RowRun> runs;
+  for (const auto& r : s.vruns) {
+    const int64_t a = std::max(lo, r.first), b = std::min(hi, r.second);
+    if (a < b) runs.push_back({a, b});
   }
   return runs;
+}
+
+// Rows of ref group g0 (its first frame) of a sample.
+RowRun group_rows(const SampleLayout& s, int32_t g0) {
+  return {int64_t(g0) * s.F, int64_t(std::min(s.ref_frames, g0 + s.group)) * s.F};
 }
 
 // Gen frames [f0, f1) a gen frame t sees under the sample's temporal window.
@@ -102,9 +108,23 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
     s.R = int64_t(g.ref_frames) * s.F;
     s.ref_frames = g.ref_frames;
     s.group = g.group_frames;
-    s.valid.assign(g.ref_frames, 1);
-    if (g.ref_frame_valid)
-      for (int32_t f = 0; f < g.ref_frames; ++f) s.valid[f] = g.ref_frame_valid[f] ? 1 : 0;
+    // runs of valid ref rows from the frame mask and the token mask
+    s.vruns.clear();
+    int64_t open = -1;  // first row of the run being extended, -1 = none
+    for (int32_t f = 0; f < g.ref_frames; ++f) {
+      const bool fv = !g.ref_frame_valid || g.ref_frame_valid[f];
+      for (int64_t j = 0; j < s.F; ++j) {
+        const int64_t r = int64_t(f) * s.F + j;
+        const bool tv = fv && (!g.ref_token_valid || g.ref_token_valid[r]);
+        if (tv && open < 0) open = r;
+        if (!tv && open >= 0) {
+          s.vruns.push_back({open, r});
+          open = -1;
+        }
+        if (!g.ref_token_valid && !fv) break;  // a frame mask alone: skip the frame's rows
+      }
+    }
+    if (open >= 0) s.vruns.push_back({open, s.R});
     s.gen_off = L.sum_gen;
     s.ref_off = L.sum_ref;
     L.sum_gen += s.G;
@@ -121,8 +141,9 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
 void closed_form_pairs(const Layout& L, int64_t* gen_pairs, int64_t* ref_pairs) {
   int64_t gp = 0, rp = 0;
   for (const SampleLayout& s : L.samples) {
-    int64_t valid_frames = std::accumulate(s.valid.begin(), s.valid.end(), int64_t(0));
-    gp += s.G * valid_frames * s.F;
+    int64_t valid_rows = 0;
+    for (const auto& r : s.vruns) valid_rows += r.second - r.first;
+    gp += s.G * valid_rows;
     if (s.window < 0) {
       gp += s.G * s.G;
     } else {
@@ -132,9 +153,10 @@ void closed_form_pairs(const Layout& L, int64_t* gen_pairs, int64_t* ref_pairs) 
       }
     }
     for (int32_t g0 = 0; g0 < s.ref_frames; g0 += s.group) {
+      const RowRun gr = group_rows(s, g0);
       int64_t n = 0;
-      for (int32_t f = g0; f < std::min(s.ref_frames, g0 + s.group); ++f) n += s.valid[f];
-      rp += (n * s.F) * (n * s.F);
+      for (const RowRun& r : valid_runs(s, gr.r0, gr.r1)) n += r.r1 - r.r0;
+      rp += n * n;
     }
   }
   if (gen_pairs) *gen_pairs = gp;
@@ -205,12 +227,12 @@ void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
     const SampleLayout& sm = L.samples[b];
     // gen queries: gen keys (all, or the frames of the temporal window) + every valid ref run.
     // With a window, query tiles are cut per gen frame so that a tile shares one key set.
-    const std::vector<Run> ref_runs = valid_runs(sm, 0, sm.ref_frames);
+    const std::vector<RowRun> ref_runs = valid_runs(sm, 0, sm.R);
     auto gen_class = [&](int64_t row0, int64_t rows, int64_t key0, int64_t keys) {
       TileClass c{0, row0, rows, int32_t(s->spans.size()), 0, b, 0};
       s->spans.push_back({0, int32_t(key0), int32_t(keys), 0});
-      for (const Run& r : ref_runs)
-        s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
+      for (const RowRun& r : ref_runs)
+        s->spans.push_back({1, int32_t(sm.ref_off + r.r0), int32_t(r.r1 - r.r0), 0});
       c.span_cnt = int32_t(s->spans.size()) - c.span_off;
       classes.push_back(c);
     };
@@ -225,13 +247,14 @@ void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
     if (L.gen_only) continue;
     // ref queries: per group, keys = valid runs of the group; query tiles per valid run
     for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
-      std::vector<Run> runs = valid_runs(sm, g0, std::min(sm.ref_frames, g0 + sm.group));
+      const RowRun gr = group_rows(sm, g0);
+      std::vector<RowRun> runs = valid_runs(sm, gr.r0, gr.r1);
       if (runs.empty()) continue;
       int32_t off = int32_t(s->spans.size());
-      for (const Run& r : runs)
-        s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
-      for (const Run& r : runs)
-        classes.push_back({1, sm.ref_off + r.f0 * sm.F, (r.f1 - r.f0) * sm.F, off, int32_t(runs.size()), b, 0});
+      for (const RowRun& r : runs)
+        s->spans.push_back({1, int32_t(sm.ref_off + r.r0), int32_t(r.r1 - r.r0), 0});
+      for (const RowRun& r : runs)
+        classes.push_back({1, sm.ref_off + r.r0, r.r1 - r.r0, off, int32_t(runs.size()), b, 0});
     }
   }
   std::vector<std::pair<int64_t, WorkItem>> v;
@@ -260,18 +283,19 @@ void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
         classes.push_back({0, sm.gen_off + t * sm.Fg, sm.Fg, gq, 1, b, 0});
       }
     }
-    // ref keys of a valid frame: gen queries + ref queries of the valid frames of its group
+    // valid ref keys: gen queries + the valid ref queries of their group
     for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
-      std::vector<Run> runs = valid_runs(sm, g0, std::min(sm.ref_frames, g0 + sm.group));
+      const RowRun gr = group_rows(sm, g0);
+      std::vector<RowRun> runs = valid_runs(sm, gr.r0, gr.r1);
       if (runs.empty()) continue;
       int32_t off = int32_t(s->spans.size());
       s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
       if (!L.gen_only)
-        for (const Run& r : runs)
-          s->spans.push_back({1, int32_t(sm.ref_off + r.f0 * sm.F), int32_t((r.f1 - r.f0) * sm.F), 0});
+        for (const RowRun& r : runs)
+          s->spans.push_back({1, int32_t(sm.ref_off + r.r0), int32_t(r.r1 - r.r0), 0});
       const int32_t cnt = int32_t(s->spans.size()) - off;
-      for (const Run& r : runs)
-        classes.push_back({1, sm.ref_off + r.f0 * sm.F, (r.f1 - r.f0) * sm.F, off, cnt, b, 0});
+      for (const RowRun& r : runs)
+        classes.push_back({1, sm.ref_off + r.r0, r.r1 - r.r0, off, cnt, b, 0});
     }
   }
   std::vector<std::pair<int64_t, WorkItem>> v;
@@ -287,15 +311,13 @@ void build_plan(const Layout& L, Plan* plan) {
   build_query_major(L, kDqQueryTile, kDqKeyStep, &plan->dq);
   build_key_major(L, kDkvKeyTile, kDkvQueryStep, &plan->dkv);
   plan->fill.clear();
-  for (const SampleLayout& sm : L.samples) {
-    int32_t f = 0;
-    while (f < sm.ref_frames) {
-      if (sm.valid[f]) { ++f; continue; }
-      int32_t g = f;
-      while (g < sm.ref_frames && !sm.valid[g]) ++g;
-      plan->fill.push_back({1, int32_t(sm.ref_off + f * sm.F), int32_t((g - f) * sm.F), 0});
-      f = g;
+  for (const SampleLayout& sm : L.samples) {  // the gaps between valid ref runs
+    int64_t r = 0;
+    for (const auto& v : sm.vruns) {
+      if (v.first > r) plan->fill.push_back({1, int32_t(sm.ref_off + r), int32_t(v.first - r), 0});
+      r = v.second;
     }
+    if (r < sm.R) plan->fill.push_back({1, int32_t(sm.ref_off + r), int32_t(sm.R - r), 0});
   }
 }
 
@@ -316,7 +338,8 @@ std::string layout_key(const Layout& L) {
   put(L.batch); put(L.heads); put(L.head_dim); put(L.gen_only ? 1 : 0);
   for (const SampleLayout& s : L.samples) {
     put(s.G); put(s.R); put(s.F); put(s.Fg); put(s.ref_frames); put(s.group); put(s.window);
-    k.append(reinterpret_cast<const char*>(s.valid.data()), s.valid.size());
+    put(int64_t(s.vruns.size()));
+    for (const auto& r : s.vruns) { put(r.first); put(r.second); }
   }
   return k;
 }

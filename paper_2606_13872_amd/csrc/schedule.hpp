@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "sra.h"
@@ -18,7 +19,9 @@ struct SampleLayout {
   int64_t gen_off = 0, ref_off = 0;   // first packed row of the sample in each stream
   int32_t gen_frames = 0, ref_frames = 0, group = 1;
   int32_t window = -1;                // gen-gen temporal window in frames; -1 = none
-  std::vector<uint8_t> valid;         // per ref frame, 0/1
+  // maximal runs [first, last) of valid ref token rows (sample-relative): a token is valid when
+  // its frame is and, with a token mask, its own entry is
+  std::vector<std::pair<int64_t, int64_t>> vruns;
 };
 
 struct Layout {

@@ -12,6 +12,8 @@ import os
 import re
 from typing import Dict, Optional, Sequence, Tuple
 
+import numpy as np
+
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsra.so")
 HEADER_PATH = os.path.join(os.path.dirname(_HERE), "include", "sra.h")
@@ -39,6 +41,7 @@ class _SampleGeom(ctypes.Structure):
         ("gen_frames", ctypes.c_int32), ("gen_h", ctypes.c_int32), ("gen_w", ctypes.c_int32),
         ("ref_frames", ctypes.c_int32), ("ref_h", ctypes.c_int32), ("ref_w", ctypes.c_int32),
         ("group_frames", ctypes.c_int32), ("gen_window", ctypes.c_int32), ("ref_frame_valid", ctypes.c_void_p),
+        ("ref_token_valid", ctypes.c_void_p),
     ]
 
 
@@ -124,15 +127,21 @@ class Problem:
         if any(getattr(g, "gen_window", None) is not None for g in self.samples):
             flags |= FLAG_GEN_WINDOW
         for i, g in enumerate(self.samples):
-            v = getattr(g, "frame_valid", None)
-            ptr = None
-            if v is not None:
-                buf = (ctypes.c_uint8 * max(1, len(v)))(*[1 if x else 0 for x in v])
-                self._valid.append(buf)
-                ptr = ctypes.cast(buf, ctypes.c_void_p)
+            ptrs = []
+            for name, n in (("frame_valid", g.ref_frames), ("ref_token_valid", g.ref_frames * g.ref_h * g.ref_w)):
+                v = getattr(g, name, None)
+                if v is None:
+                    ptrs.append(None)
+                    continue
+                a = np.ascontiguousarray(np.asarray(v).astype(bool).astype(np.uint8))
+                if a.shape != (n,):
+                    raise ValueError(f"sample {i}: {name} needs {n} entries, got {a.shape}")
+                self._valid.append(a)  # the library reads these host bytes during the call
+                ptrs.append(a.ctypes.data_as(ctypes.c_void_p))
             w = getattr(g, "gen_window", None)
             self._geoms[i] = _SampleGeom(g.gen_frames, g.gen_h, g.gen_w, g.ref_frames, g.ref_h, g.ref_w,
-                                         getattr(g, "group_frames", 1), g.gen_frames if w is None else int(w), ptr)
+                                         getattr(g, "group_frames", 1), g.gen_frames if w is None else int(w),
+                                         ptrs[0], ptrs[1])
         self.c = _Problem(len(self.samples), heads, head_dim, 0.0 if scale is None else float(scale),
                           ctypes.cast(self._geoms, ctypes.POINTER(_SampleGeom)),
                           gen_token_stride, ref_token_stride, flags)

@@ -17,6 +17,8 @@ Workload recipes (the paper gives no SRA workload; these mirror its video shapes
               numpy default_rng(13872).choice([2, 4, 8, 12], 4).
   * varlen_window : the varlen batch with a +-1 latent-frame window on gen-gen attention
               (the refiner's sparse temporal attention), seed 5.
+  * varlen_tokens : the varlen batch with a reference token mask per sample from
+              box_token_mask(r, 68, 120, 13872 + i) (invalid boxes and frames), seed 6.
 Every value is an iid N(0,1) fp32 draw rounded to bf16 (round-to-nearest-even).
 Draw order: q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, do_gen, do_ref.
 """
@@ -37,7 +39,9 @@ class SampleGeom:
     group of reference queries. frame_valid (None = all valid) marks reference frames
     that take part at all (e.g. frames where the face is visible). gen_window (None = no
     window) limits which generation keys a generation query sees to the latent frames within
-    that many frames of its own (the refiner's sparse temporal attention).
+    that many frames of its own (the refiner's sparse temporal attention). ref_token_valid
+    (None = every token of a valid frame) marks single reference tokens, frame-major, one
+    entry per reference token; a token takes part when its frame and its own entry are valid.
     """
 
     gen_frames: int
@@ -49,6 +53,7 @@ class SampleGeom:
     group_frames: int = 1
     frame_valid: Optional[Sequence[int]] = field(default=None)
     gen_window: Optional[int] = None
+    ref_token_valid: Optional[Sequence[int]] = field(default=None)
 
     @property
     def n_gen(self) -> int:
@@ -72,6 +77,29 @@ class Workload:
 VARLEN_REF_FRAMES = [int(x) for x in np.random.default_rng(13872).choice([2, 4, 8, 12], size=4)]
 
 
+def box_token_mask(ref_frames: int, ref_h: int, ref_w: int, seed: int, p_frame_invalid: float = 0.1,
+                   p_box: float = 0.6, box_area=(0.1, 0.4)) -> tuple:
+    """A reference token mask with the structure of invalid regions in video: per frame, the
+    whole frame is invalid with probability p_frame_invalid, else with probability p_box one
+    axis-aligned box covering box_area (fraction range) of the frame is invalid, else the
+    frame is fully valid. Frame-major, 1 = valid. Drawn from numpy default_rng(seed)."""
+    rng = np.random.default_rng(seed)
+    m = np.ones((ref_frames, ref_h, ref_w), dtype=np.uint8)
+    for f in range(ref_frames):
+        u = rng.random()
+        if u < p_frame_invalid:
+            m[f] = 0
+        elif u < p_frame_invalid + p_box:
+            area = rng.uniform(*box_area)
+            aspect = rng.uniform(0.5, 2.0)
+            bh = int(np.clip(round(np.sqrt(area * ref_h * ref_w * aspect)), 1, ref_h))
+            bw = int(np.clip(round(area * ref_h * ref_w / bh), 1, ref_w))
+            y0 = int(rng.integers(0, ref_h - bh + 1))
+            x0 = int(rng.integers(0, ref_w - bw + 1))
+            m[f, y0:y0 + bh, x0:x0 + bw] = 0
+    return tuple(int(x) for x in m.reshape(-1))
+
+
 def workload(name: str) -> Workload:
     if name == "tiny":
         return Workload(name, [SampleGeom(2, 8, 8, 4, 8, 8)], 1, 64, 0, False)
@@ -89,6 +117,11 @@ def workload(name: str) -> Workload:
         # the same packed batch with the refiner's temporal window: +-1 latent frame
         return Workload(name, [SampleGeom(5, 68, 120, r, 68, 120, gen_window=1) for r in VARLEN_REF_FRAMES],
                         24, 128, 5, True)
+    if name == "varlen_tokens":
+        # the varlen batch with token-level validity: invalid boxes and frames in the reference
+        return Workload(name, [SampleGeom(5, 68, 120, r, 68, 120,
+                                          ref_token_valid=box_token_mask(r, 68, 120, 13872 + i))
+                               for i, r in enumerate(VARLEN_REF_FRAMES)], 24, 128, 6, True)
     raise KeyError(name)
 
 

@@ -2,7 +2,8 @@
 
 Counts come from the CPU oracle's explicit visibility mask (built in row blocks), so
 they follow the visibility rule of Avatar V §1 (contributions), §2.1 and §4.3, with one
-reference latent frame per self-attention group. Run from the repository root:
+reference latent frame per self-attention group (and, for varlen_window, the temporal window
+of §2.4; for varlen_tokens, the reference token masks of that workload). Run from the repository root:
     python tests/golden/make_pair_counts.py
 """
 import json
@@ -16,7 +17,7 @@ sys.path.insert(0, ROOT)
 import oracle  # noqa: E402
 from sra_inputs import SWEEP_POINTS, workload  # noqa: E402
 
-names = ["tiny", "480p"] + [f"sweep_{n}" for n in SWEEP_POINTS] + ["720p", "varlen"]
+names = ["tiny", "480p"] + [f"sweep_{n}" for n in SWEEP_POINTS] + ["720p", "varlen", "varlen_window", "varlen_tokens"]
 out = {"_source": "oracle.pair_counts over the explicit mask; per head, summed over samples"}
 for name in names:
     w = workload(name)

@@ -110,8 +110,9 @@ def test_window_flag_constant_and_struct_layout():
     text = open(sra.HEADER_PATH).read()
     m = re.search(r"SRA_FLAG_GEN_WINDOW\s*=\s*(\d+)u", text)
     assert m and int(m.group(1)) == sra.FLAG_GEN_WINDOW
-    # gen_window fills the padding before the pointer: the struct keeps its size
-    assert ctypes.sizeof(sra._SampleGeom) == 40 and sra._SampleGeom.ref_frame_valid.offset == 32
+    # gen_window fills the padding before the first pointer; the token mask pointer follows it
+    assert ctypes.sizeof(sra._SampleGeom) == 48 and sra._SampleGeom.ref_frame_valid.offset == 32
+    assert sra._SampleGeom.ref_token_valid.offset == 40
     bad = SampleGeom(3, 2, 2, 1, 2, 2, gen_window=-1)
     with pytest.raises(sra.SRAError) as e:
         sra.Problem([bad], 1, 64).workspace_size(False)

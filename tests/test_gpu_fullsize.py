@@ -88,7 +88,7 @@ def _close(name, got, want):
     assert rel <= REL, f"{name}: relative err {rel:.3e}"
 
 
-@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "varlen", "varlen_window"])
+@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "varlen", "varlen_window", "varlen_tokens"])
 def test_fullsize_forward_sampled_rows(name):
     w = workload(name)
     x = _inputs(w, grads=False)
@@ -105,7 +105,10 @@ def test_fullsize_forward_sampled_rows(name):
             got_o = _gpu_rows(o_gen[:, h], o_ref[:, h], go, ro, b, geom.n_gen, rows)
             _close(f"{name} O h{h} b{b}", got_o, want_o)
             got_l = _gpu_lse_rows(l_gen, l_ref, go, ro, b, geom.n_gen, h, rows)
-            err = np.abs(got_l - want_lse).max()
+            # rows of invalid reference tokens: LSE = -inf on both sides
+            assert np.array_equal(np.isneginf(got_l), np.isneginf(want_lse)), f"{name} LSE -inf rows h{h} b{b}"
+            fin = np.isfinite(want_lse)
+            err = np.abs(got_l[fin] - want_lse[fin]).max()
             assert err <= LSE_ABS, f"{name} LSE h{h} b{b}: {err:.3e}"
 
 
@@ -129,9 +132,21 @@ def test_fullsize_dq_sampled_rows(name):
         _close(f"{name} dQ b{b}", got, want)
 
 
-@pytest.mark.parametrize("name", ["720p", "varlen", "varlen_window"])
+def _ref_token_ok(geom):
+    """Per reference token: its frame is valid and so is its own entry of the token mask."""
+    F = geom.ref_h * geom.ref_w
+    ok = np.ones(geom.n_ref, dtype=bool)
+    if geom.frame_valid is not None:
+        ok &= np.repeat(np.asarray(geom.frame_valid, dtype=bool), F)
+    if geom.ref_token_valid is not None:
+        ok &= np.asarray(geom.ref_token_valid, dtype=bool)
+    return ok
+
+
+@pytest.mark.parametrize("name", ["720p", "varlen", "varlen_window", "varlen_tokens"])
 def test_fullsize_zero_keys_count_law(name):
-    """K = 0 makes every visible logit 0, so LSE = ln(number of visible keys) for every row."""
+    """K = 0 makes every visible logit 0, so LSE = ln(number of visible keys) for every row
+    (and -inf for rows of invalid reference tokens)."""
     w = workload(name)
     x = _inputs(w, grads=False)
     x["k_gen"].zero_()
@@ -143,13 +158,19 @@ def test_fullsize_zero_keys_count_law(name):
         F = geom.ref_h * geom.ref_w
         lg = l_gen[:, go[b]:go[b + 1]].double()
         fg, T, w = geom.gen_h * geom.gen_w, geom.gen_frames, geom.gen_window
+        ok = _ref_token_ok(geom)
         for t in range(T):
             seen = T if w is None else min(T - 1, t + w) - max(0, t - w) + 1
-            cnt = seen * fg + geom.n_ref
+            cnt = seen * fg + int(ok.sum())
             assert torch.all((lg[:, t * fg:(t + 1) * fg] - math.log(cnt)).abs() < 1e-5), f"gen frame {t}, sample {b}"
         if geom.n_ref:
-            lr = l_ref[:, ro[b]:ro[b + 1]]
-            assert torch.all((lr.double() - math.log(F * geom.group_frames)).abs() < 1e-5), f"ref rows, sample {b}"
+            gsz = F * geom.group_frames
+            per_group = np.add.reduceat(ok.astype(np.int64), np.arange(0, geom.n_ref, gsz))
+            want = np.where(ok, np.log(np.maximum(np.repeat(per_group, gsz)[:geom.n_ref], 1)), -np.inf)
+            lr = l_ref[:, ro[b]:ro[b + 1]].double().cpu().numpy()
+            assert np.array_equal(np.isneginf(lr), np.broadcast_to(np.isneginf(want), lr.shape)), f"ref -inf rows, sample {b}"
+            fin = np.isfinite(want)
+            assert np.all(np.abs(lr[:, fin] - want[fin]) < 1e-5), f"ref rows, sample {b}"
 
 
 IDENTITY_REL = 0.04

@@ -12,7 +12,7 @@ import torch
 
 import oracle
 from paper_2606_13872_amd import sra
-from sra_inputs import SampleGeom, make_inputs, to_numpy64
+from sra_inputs import SampleGeom, box_token_mask, make_inputs, to_numpy64
 
 pytestmark = pytest.mark.gpu
 
@@ -84,6 +84,10 @@ def check_against_oracle(samples, H, d, seed, rms=False, scale=None, backward=Tr
     return x, got
 
 
+def _rand_tokens(n, seed, p):
+    return tuple(int(x) for x in (np.random.default_rng(seed).random(n) >= p))
+
+
 CASES = {
     # name: (samples, H, d, seed, rms)
     "tiny": ([SampleGeom(2, 8, 8, 4, 8, 8)], 1, 64, 0, False),
@@ -104,6 +108,17 @@ CASES = {
                        SampleGeom(3, 10, 7, 3, 5, 6, group_frames=2, gen_window=1),
                        SampleGeom(2, 9, 9, 2, 9, 9)], 2, 128, 27, False),
     "d64_window": ([SampleGeom(6, 9, 9, 2, 9, 9, gen_window=2)], 2, 64, 28, False),
+    # token-level validity (§4.3 invalid tokens): box masks, random masks, with frame masks,
+    # groups and windows; runs of valid tokens become spans and query/key tiles
+    "tokens_box": ([SampleGeom(2, 16, 20, 4, 16, 20, ref_token_valid=box_token_mask(4, 16, 20, 40))],
+                   2, 128, 29, True),
+    "tokens_random": ([SampleGeom(1, 12, 16, 3, 10, 12, group_frames=3,
+                                  ref_token_valid=_rand_tokens(360, 41, 0.4))], 2, 128, 30, False),
+    "tokens_varlen": ([SampleGeom(2, 9, 15, 3, 9, 15, frame_valid=[1, 0, 1], ref_token_valid=box_token_mask(3, 9, 15, 42)),
+                       SampleGeom(3, 8, 8, 2, 7, 7, gen_window=1, ref_token_valid=_rand_tokens(98, 43, 0.2)),
+                       SampleGeom(1, 7, 7, 2, 5, 5, ref_token_valid=(0,) * 50)], 2, 128, 31, True),
+    "d64_tokens": ([SampleGeom(2, 10, 10, 4, 9, 9, group_frames=2, ref_token_valid=box_token_mask(4, 9, 9, 44))],
+                   2, 64, 32, False),
 }
 
 

@@ -98,6 +98,34 @@ def mask_window_ignored(geom, rows=None):
     return _orig_mask(g, rows)
 
 
+_orig_token_valid = so.token_valid
+
+
+def tok_ignored(geom):
+    # the token mask is dropped: only the frame mask counts
+    G, R, F = so.sample_sizes(geom)
+    return np.repeat(so.frame_valid(geom), F) if R > 0 else np.zeros(0, dtype=bool)
+
+
+def tok_shifted(geom):
+    # wrong index: the mask of token j is read at j + 1
+    return np.roll(_orig_token_valid(geom), -1)
+
+
+def mask_token_keys_only(geom, rows=None):
+    # invalid tokens are dropped as keys but still answer as queries (in valid frames)
+    M = _orig_mask(geom, rows)
+    G, R, F = so.sample_sizes(geom)
+    tv = _orig_token_valid(geom)
+    fv = np.repeat(so.frame_valid(geom), F)
+    r = np.arange(G + R) if rows is None else np.asarray(rows)
+    grp = (np.arange(R) // F) // geom.group_frames
+    for i, q in enumerate(r):
+        if q >= G and fv[q - G] and not tv[q - G]:
+            M[i, G:] = tv & (grp == grp[q - G])
+    return M
+
+
 def rows_no_scale(q, k, v, M, scale):
     return _orig_rows(q, k, v, M, 1.0)
 
@@ -144,6 +172,9 @@ def _all_forward_pins():
     pins.test_brute_force_quadruple_loop(2, 1)
     pins.test_window_zero_without_reference_is_per_frame_attention()
     pins.test_window_pair_count_closed_form()
+    pins.test_token_mask_predicates_pair_counts_and_closed_form()
+    for geom in pins.TOKEN_GEOMS[:3]:
+        pins.test_invalid_tokens_are_dropped_keys_and_dead_queries(geom)
 
 
 def _all_backward_pins():
@@ -159,6 +190,9 @@ def _all_backward_pins():
     ("visibility_mask", mask_ignores_validity, "fwd"),
     ("visibility_mask", mask_window_strict, "fwd"),
     ("visibility_mask", mask_window_ignored, "fwd"),
+    ("token_valid", tok_ignored, "fwd"),
+    ("token_valid", tok_shifted, "fwd"),
+    ("visibility_mask", mask_token_keys_only, "fwd"),
     ("attention_rows", rows_no_scale, "fwd"),
     ("attention_rows", rows_lse_without_max, "fwd"),
     ("attention_backward_full", bwd_sign, "bwd"),

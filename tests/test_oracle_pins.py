@@ -27,11 +27,19 @@ def rand_inputs(samples, H, d, rng=None, dtype=np.float64, grads=False):
 
 
 # --------------------------------------------------------------------- predicates (independent)
+def ref_token_ok(geom, j):
+    """Reference token j takes part: its frame is valid and, with a token mask, so is it."""
+    F = geom.ref_h * geom.ref_w
+    if geom.frame_valid is not None and not geom.frame_valid[j // F]:
+        return False
+    tv = getattr(geom, "ref_token_valid", None)
+    return tv is None or bool(tv[j])
+
+
 def pred_visible(geom, qi, ki):
     """Visibility of one (query, key) pair written as predicates, [gen ; ref] indexing."""
     G = geom.gen_frames * geom.gen_h * geom.gen_w
     F = geom.ref_h * geom.ref_w
-    valid = [True] * geom.ref_frames if geom.frame_valid is None else [bool(x) for x in geom.frame_valid]
     q_is_gen, k_is_gen = qi < G, ki < G
     if q_is_gen and k_is_gen:
         w = getattr(geom, "gen_window", None)
@@ -40,29 +48,31 @@ def pred_visible(geom, qi, ki):
         fg = geom.gen_h * geom.gen_w
         return abs(qi // fg - ki // fg) <= w
     if q_is_gen:
-        return valid[(ki - G) // F]
+        return ref_token_ok(geom, ki - G)
     if k_is_gen:
         return False
     fq, fk = (qi - G) // F, (ki - G) // F
-    return valid[fq] and valid[fk] and (fq // geom.group_frames) == (fk // geom.group_frames)
+    return (ref_token_ok(geom, qi - G) and ref_token_ok(geom, ki - G)
+            and (fq // geom.group_frames) == (fk // geom.group_frames))
 
 
 def visible_count_closed_form(geom, qi):
     G = geom.gen_frames * geom.gen_h * geom.gen_w
     F = geom.ref_h * geom.ref_w
-    valid = [True] * geom.ref_frames if geom.frame_valid is None else [bool(x) for x in geom.frame_valid]
+    R = geom.ref_frames * F
+    n_valid = sum(ref_token_ok(geom, j) for j in range(R))
     if qi < G:
         w = getattr(geom, "gen_window", None)
         if w is None:
-            return G + F * sum(valid)
+            return G + n_valid
         t, T = qi // (geom.gen_h * geom.gen_w), geom.gen_frames
-        return (min(T - 1, t + w) - max(0, t - w) + 1) * geom.gen_h * geom.gen_w + F * sum(valid)
-    f = (qi - G) // F
-    if not valid[f]:
+        return (min(T - 1, t + w) - max(0, t - w) + 1) * geom.gen_h * geom.gen_w + n_valid
+    j = qi - G
+    if not ref_token_ok(geom, j):
         return 0
     g = geom.group_frames
-    grp = f // g
-    return F * sum(valid[grp * g:(grp + 1) * g])
+    lo, hi = (j // F) // g * g * F, min(R, ((j // F) // g + 1) * g * F)
+    return sum(ref_token_ok(geom, i) for i in range(lo, hi))
 
 
 def torch_sdpa64(q, k, v, scale):
@@ -467,3 +477,111 @@ def test_window_pair_count_closed_form():
         nv = geom.ref_frames if geom.frame_valid is None else sum(geom.frame_valid)
         want = sum(fg * fg * (min(T - 1, t + w) - max(0, t - w) + 1) for t in range(T)) + geom.n_gen * F * nv
         assert oracle.pair_counts([geom], block_rows=7)[0] == want
+
+
+# --------------------------------------------------------------------- token-level validity
+def _token_mask(geom, seed, p=0.3):
+    """Random reference token mask (1 = valid) with about a fraction p of invalid tokens."""
+    rng = np.random.default_rng(seed)
+    return tuple(int(x) for x in (rng.random(geom.n_ref) >= p))
+
+
+def _with_tokens(geom, seed, p=0.3):
+    import dataclasses
+    return dataclasses.replace(geom, ref_token_valid=_token_mask(geom, seed, p))
+
+
+TOKEN_GEOMS = [
+    _with_tokens(SampleGeom(2, 3, 5, 4, 3, 4), 11),
+    _with_tokens(SampleGeom(3, 2, 4, 5, 2, 5, frame_valid=[1, 0, 1, 1, 0]), 12),
+    _with_tokens(SampleGeom(1, 4, 4, 6, 3, 3, group_frames=2, frame_valid=[1, 1, 0, 1, 1, 1]), 13, 0.5),
+    _with_tokens(SampleGeom(3, 2, 2, 3, 2, 2, group_frames=3, gen_window=1), 14),
+    SampleGeom(2, 2, 3, 3, 2, 3, ref_token_valid=(0,) * 18),           # every reference token invalid
+    SampleGeom(1, 2, 2, 2, 2, 2, ref_token_valid=(1, 1, 1, 1, 0, 1, 1, 1)),  # one invalid token
+]
+
+
+def test_token_mask_predicates_pair_counts_and_closed_form():
+    for geom in TOKEN_GEOMS:
+        M = oracle.visibility_mask(geom)
+        n = geom.n_gen + geom.n_ref
+        P = np.array([[pred_visible(geom, i, j) for j in range(n)] for i in range(n)])
+        assert np.array_equal(M, P)
+        gp, rp = oracle.pair_counts([geom], block_rows=7)
+        G = geom.n_gen
+        assert gp == sum(visible_count_closed_form(geom, q) for q in range(G))
+        assert rp == sum(visible_count_closed_form(geom, q) for q in range(G, n))
+
+
+@pytest.mark.parametrize("fv", [[1, 0, 1, 1], [0, 0, 1, 0], [1, 1, 1, 1]])
+def test_token_mask_constant_per_frame_equals_the_frame_mask(fv):
+    """A token mask that repeats a frame mask over each frame's tokens is that frame mask."""
+    a = SampleGeom(2, 2, 3, 4, 2, 3, group_frames=2, frame_valid=fv)
+    b = SampleGeom(2, 2, 3, 4, 2, 3, group_frames=2, ref_token_valid=tuple(np.repeat(fv, 6)))
+    x = rand_inputs([a], 2, 8, grads=True)
+    fa, fb = oracle.sra_forward(x, [a]), oracle.sra_forward(x, [b])
+    for u, w in zip(fa, fb):
+        assert np.array_equal(u, w)
+    ga, gb = oracle.sra_backward(x, [a]), oracle.sra_backward(x, [b])
+    for k in ga:
+        assert np.array_equal(ga[k], gb[k])
+
+
+@pytest.mark.parametrize("geom", TOKEN_GEOMS)
+def test_invalid_tokens_are_dropped_keys_and_dead_queries(geom):
+    """Gen rows = dense attention over gen keys (window frames) and the valid reference tokens;
+    valid ref rows = dense attention over the valid tokens of their group; invalid ref rows are
+    O = 0, LSE = -inf (library SDPA over explicit key lists)."""
+    H, d = 2, 8
+    x = rand_inputs([geom], H, d)
+    o_gen, o_ref, lse_gen, lse_ref = oracle.sra_forward(x, [geom])
+    G, R, F = geom.n_gen, geom.n_ref, geom.ref_h * geom.ref_w
+    ok = np.array([ref_token_ok(geom, j) for j in range(R)], dtype=bool)
+    fg = geom.gen_h * geom.gen_w
+    w = geom.gen_window
+    for h in range(H):
+        for qi in range(G):
+            gk = np.arange(G) if w is None else np.nonzero(np.abs(np.arange(G) // fg - qi // fg) <= w)[0]
+            k = np.concatenate([x["k_gen"][gk, h], x["k_ref"][ok, h]])
+            v = np.concatenate([x["v_gen"][gk, h], x["v_ref"][ok, h]])
+            o, lse = torch_sdpa64(x["q_gen"][qi:qi + 1, h], k, v, 1 / math.sqrt(d))
+            np.testing.assert_allclose(o_gen[qi, h], o[0], rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(lse_gen[h, qi], lse[0], rtol=1e-12, atol=1e-12)
+        g = geom.group_frames
+        for j in range(R):
+            if not ok[j]:
+                assert np.all(o_ref[j, h] == 0) and np.isneginf(lse_ref[h, j])
+                continue
+            grp = (j // F) // g
+            keys = [i for i in range(grp * g * F, min(R, (grp + 1) * g * F)) if ok[i]]
+            o, lse = torch_sdpa64(x["q_ref"][j:j + 1, h], x["k_ref"][keys, h], x["v_ref"][keys, h], 1 / math.sqrt(d))
+            np.testing.assert_allclose(o_ref[j, h], o[0], rtol=1e-12, atol=1e-12)
+            np.testing.assert_allclose(lse_ref[h, j], lse[0], rtol=1e-12, atol=1e-12)
+
+
+def test_token_mask_backward_finite_differences_and_dead_rows():
+    geom = SampleGeom(1, 2, 2, 3, 2, 2, group_frames=2, frame_valid=[1, 1, 0],
+                      ref_token_valid=(1, 0, 1, 1, 0, 1, 1, 1, 1, 1, 1, 1))
+    H, d = 1, 4
+    rng = np.random.default_rng(21)
+    x = rand_inputs([geom], H, d, rng=rng)
+    W = {"gen": rng.standard_normal((geom.n_gen, H, d)), "ref": rng.standard_normal((geom.n_ref, H, d))}
+    x["do_gen"], x["do_ref"] = W["gen"], W["ref"]
+    g = oracle.sra_backward(x, [geom])
+    ok = np.array([ref_token_ok(geom, j) for j in range(geom.n_ref)])
+    for nm in ("dq_ref", "dk_ref", "dv_ref"):
+        assert np.all(g[nm][~ok] == 0)
+    eps = 1e-6
+    for name in ("q_gen", "k_ref", "v_ref", "q_ref"):
+        grad = g["d" + name]
+        num = np.zeros_like(grad)
+        for idx in np.ndindex(*x[name].shape):
+            old = x[name][idx]
+            x[name][idx] = old + eps
+            lp = _loss(x, geom, W)
+            x[name][idx] = old - eps
+            lm = _loss(x, geom, W)
+            x[name][idx] = old
+            num[idx] = (lp - lm) / (2 * eps)
+        err = np.abs(num - grad).max() / max(1e-12, np.abs(num).max())
+        assert err < 1e-6, (name, err)

@@ -13,9 +13,14 @@ import pytest
 
 import oracle
 from paper_2606_13872_amd import sra
-from sra_inputs import SWEEP_POINTS, SampleGeom, workload
+from sra_inputs import SWEEP_POINTS, SampleGeom, box_token_mask, workload
 
 SCHEDS = [sra.SCHED_FORWARD, sra.SCHED_BWD_DQ, sra.SCHED_BWD_DKDV]
+
+
+def _rand_tokens(n, seed, p):
+    return tuple(int(x) for x in (np.random.default_rng(seed).random(n) >= p))
+
 
 GEOMS = [
     [SampleGeom(2, 8, 8, 4, 8, 8)],                                        # tiny workload shape
@@ -33,6 +38,14 @@ GEOMS = [
     [SampleGeom(6, 7, 7, 4, 5, 5, group_frames=2, frame_valid=[1, 0, 1, 1], gen_window=0),
      SampleGeom(4, 20, 15, 2, 9, 9, gen_window=2), SampleGeom(3, 6, 6, 1, 6, 6)],
     [SampleGeom(3, 10, 10, 2, 4, 4, gen_window=5)],                        # window >= all frames
+    # token-level validity: random masks, box masks, with frame masks, groups and windows
+    [SampleGeom(2, 9, 9, 4, 5, 7, ref_token_valid=_rand_tokens(4 * 35, 1, 0.3))],
+    [SampleGeom(2, 9, 9, 6, 5, 7, group_frames=2, frame_valid=[1, 0, 1, 1, 0, 1],
+                ref_token_valid=_rand_tokens(6 * 35, 2, 0.5))],
+    [SampleGeom(1, 8, 8, 5, 8, 8, ref_token_valid=box_token_mask(5, 8, 8, 3)),
+     SampleGeom(3, 6, 6, 3, 9, 9, group_frames=3, gen_window=1, ref_token_valid=box_token_mask(3, 9, 9, 4)),
+     SampleGeom(2, 5, 5, 2, 4, 4, ref_token_valid=(0,) * 32)],
+    [SampleGeom(1, 6, 6, 3, 6, 6, ref_token_valid=tuple([0] * 36 + [1] * 35 + [0] + [1] * 36))],
 ]
 
 
