@@ -32,7 +32,7 @@ CSRC = os.path.join(ROOT, "paper_2606_13872_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_720p.json")
 KERNEL_SYMBOLS = {"forward": "sra_fwd_kernel", "dkdv": "sra_dkv_kernel", "dq": "sra_dq_kernel",
                   "delta": "sra_delta_kernel"}
-KERNEL_SOURCES = {"forward": ["sra_fwd.hip"], "dkdv": ["sra_dkv.hip"], "dq": ["sra_bwd.hip"],
+KERNEL_SOURCES = {"forward": ["sra_fwd.hip"], "dkdv": ["sra_dkv.hip"], "dq": ["sra_dq.hip"],
                   "delta": ["sra_bwd.hip"]}
 COMMON_SOURCES = ["sra_config.h", "sra_device.h", "sra_tiles.h", "sra_kernels.h"]
 COPY_KERNEL = "neg_kernel"  # calibration: torch.neg over a float32 buffer reads and writes it once

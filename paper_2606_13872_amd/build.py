@@ -18,7 +18,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsra.so")
 
-SOURCES = ["schedule.cpp", "sra_api.cpp", "sra_fwd.hip", "sra_bwd.hip", "sra_dkv.hip"]
+SOURCES = ["schedule.cpp", "sra_api.cpp", "sra_fwd.hip", "sra_bwd.hip", "sra_dq.hip", "sra_dkv.hip"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", "-Wall",
@@ -56,7 +56,7 @@ def _compile(src: str) -> str:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=5) as ex:
+    with cf.ThreadPoolExecutor(max_workers=6) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, *objs]
