@@ -27,9 +27,10 @@ COMMON = [
 # Device code only for gfx950. Packed-FP32 instructions are disabled in device code.
 HIP_FLAGS = ["-x", "hip", "--offload-arch=gfx950", "-Xclang", "-target-feature",
              "-Xclang", "-packed-fp32-ops", "-munsafe-fp-atomics"]
-# The dK/dV kernel selects its compiler-visible MFMAs in VGPR form: its AGPRs hold the dK/dV
-# sums (written by inline-assembly MFMAs), and S/dP must stay in VGPRs next to them.
-EXTRA_FLAGS = {"sra_dkv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]}
+# The dK/dV and dQ kernels select their compiler-visible MFMAs in VGPR form: their AGPRs hold
+# the gradient sums (written by inline-assembly MFMAs), and S/dP must stay in VGPRs next to them.
+_VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+EXTRA_FLAGS = {"sra_dkv.hip": _VGPR_FORM, "sra_dq.hip": _VGPR_FORM}
 COMPILE_TIMEOUT_S = 900
 
 
