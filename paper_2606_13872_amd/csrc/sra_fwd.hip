@@ -323,16 +323,34 @@ sra_fwd_kernel(FwdArgs a) {
   FullTileCursor kc, vc;  // next full tile to load for K, for V
   kc.init(sp, it.span_cnt);
   vc.init(sp, it.span_cnt);
-  auto issue_k = [&](__bf16* dst) {
-    const int64_t row0 = int64_t(kc.cur_start + kc.off) * a.in_stride[kc.cur_stream];
-    if (kc.cur_stream == 0) kl[0].issue(dst, a.k[0] + row0, wave);
-    else kl[1].issue(dst, a.k[1] + row0, wave);
+  // per-stream bases as uniform scalars and this wave's LDS slots as byte addresses, so a
+  // tile's loads need no argument reads and no generic-to-LDS address conversions
+  const uint64_t kb0 = uniform_u64(reinterpret_cast<uint64_t>(a.k[0]));
+  const uint64_t kb1 = uniform_u64(reinterpret_cast<uint64_t>(a.k[1]));
+  const uint64_t vb0 = uniform_u64(reinterpret_cast<uint64_t>(a.v[0]));
+  const uint64_t vb1 = uniform_u64(reinterpret_cast<uint64_t>(a.v[1]));
+  const int64_t st0 = a.in_stride[0], st1 = a.in_stride[1];
+  using KTL = PaddedTile<D, BK, RK>;
+  using VTL = PaddedTile<D, BK, RV>;
+  constexpr int kKFull = KTL::kInstr / kWaves, kVFull = VTL::kInstr / kWaves;
+  const bool k_extra = wave + kKFull * kWaves < KTL::kInstr;
+  const bool v_extra = wave + kVFull * kWaves < VTL::kInstr;
+  auto issue_k = [&](const __bf16* dst) __attribute__((always_inline)) {
+    const int ss = kc.cur_stream;
+    const __bf16* g = reinterpret_cast<const __bf16*>(ss ? kb1 : kb0) + int64_t(kc.cur_start + kc.off) * (ss ? st1 : st0);
+    const uint32_t la = lds_addr(dst) + wave * 1024;
+#pragma unroll
+    for (int j = 0; j < kKFull + 1; ++j)
+      if (j < kKFull || k_extra) lds_dma_x4_at(g + (ss ? kl[1].voff[j] : kl[0].voff[j]), la + j * kWaves * 1024);
     kc.advance();
   };
-  auto issue_v = [&](__bf16* dst) {
-    const int64_t row0 = int64_t(vc.cur_start + vc.off) * a.in_stride[vc.cur_stream];
-    if (vc.cur_stream == 0) vl[0].issue(dst, a.v[0] + row0, wave);
-    else vl[1].issue(dst, a.v[1] + row0, wave);
+  auto issue_v = [&](const __bf16* dst) __attribute__((always_inline)) {
+    const int ss = vc.cur_stream;
+    const __bf16* g = reinterpret_cast<const __bf16*>(ss ? vb1 : vb0) + int64_t(vc.cur_start + vc.off) * (ss ? st1 : st0);
+    const uint32_t la = lds_addr(dst) + wave * 1024;
+#pragma unroll
+    for (int j = 0; j < kVFull + 1; ++j)
+      if (j < kVFull || v_extra) lds_dma_x4_at(g + (ss ? vl[1].voff[j] : vl[0].voff[j]), la + j * kWaves * 1024);
     vc.advance();
   };
 
