@@ -217,12 +217,18 @@ sra_dkv_kernel(BwdArgs a) {
   using QTL = PaddedTile<D, BQ, RQ>;
   constexpr uint32_t kBufBytes = QTL::kElems * 2;
   constexpr int kFull = QTL::kInstr / kDkvWaves;  // load slots every wave has
-  constexpr int kStatWave = kDkvWaves - 1;         // the row statistics ride with the last wave
   const uint32_t q_lds = lds_addr(&qs[0][0]) + wave * 1024, d_lds = lds_addr(&dos[0][0]) + wave * 1024;
   const bool extra_slot = wave + kFull * kDkvWaves < QTL::kInstr;
   static_assert(BQ == 32, "one dword per lane covers both statistics of 32 rows");
-  auto issue = [&](int b) __attribute__((always_inline)) {  // the next step -> buffer b
+  float stat = 0.f;  // the row statistics a wave loads for a later step (waves take turns)
+  auto issue = [&](int b, int u) __attribute__((always_inline)) {  // step u -> buffer b
     const int ss = ld.stream();
+    if (wave == (u & 3)) {  // lanes < 32: LSE of the step's rows; the others: -D
+      const int rr = ld.start() + min(ld.off + l32, ld.len() - 1) + (ss ? hr1 : hr0);
+      const uint64_t nbs = ss ? nb1 : nb0, lbs = ss ? lb1 : lb0;
+      const uint64_t base = half ? nbs : lbs;
+      stat = reinterpret_cast<const __attribute__((address_space(1))) float*>(base)[rr];
+    }
     if (ld.off + BQ <= ld.len()) {
       const int64_t row0 = int64_t(ld.start() + ld.off);
       const __bf16* qg = reinterpret_cast<const __bf16*>(ss ? qb1 : qb0) + row0 * (ss ? qst1 : qst0);
@@ -240,17 +246,20 @@ sra_dkv_kernel(BwdArgs a) {
       tile_load_lds<D, BQ, RQ, kDkvWaves, true>(qs[b], a.q[ss], a.in_stride[ss], h, ld.start(), ld.len(), ld.off, wave);
       tile_load_lds<D, BQ, RQ, kDkvWaves, true>(dos[b], a.dout[ss], dstride, h, ld.start(), ld.len(), ld.off, wave);
     }
-    if (wave == kStatWave) {  // lanes < 32: LSE of the step's rows; the others: -D
-      const int rr = ld.start() + min(ld.off + l32, ld.len() - 1) + (ss ? hr1 : hr0);
-      const uint64_t nbs = ss ? nb1 : nb0, lbs = ss ? lb1 : lb0;
-      const uint64_t base = half ? nbs : lbs;
-      lds_dma_x1(reinterpret_cast<const float*>(base) + rr, &rstat[b][0]);
-    }
     ld.advance(BQ);
   };
+  // the loading wave stores the statistics of step u at the end of step u - 2 (they are read
+  // at step u, after the barrier of step u - 2 or u - 1)
+  auto put_stat = [&](int u) __attribute__((always_inline)) {
+    if (wave == (u & 3)) rstat[u % NB][lane] = stat;
+  };
 
-  issue(0);
-  if (T > 1) issue(1);
+  issue(0, 0);
+  put_stat(0);
+  if (T > 1) {
+    issue(1, 1);
+    put_stat(1);
+  }
   wait_vmem();
   __syncthreads();
   // step t reads buffer t % NB and loads step t + 2 into buffer (t + 2) % NB, whose last
@@ -267,14 +276,16 @@ sra_dkv_kernel(BwdArgs a) {
     const int full = len / BQ;
     for (int j = 0; j < full; ++j, ++t) {
       const int b = t % NB;
-      if (t + 2 < T) issue((t + 2) % NB);
+      if (t + 2 < T) issue((t + 2) % NB, t + 2);
       if (active) dkv_step<D, false>(st, krow, qs[b], dos[b], rstat[b], rstat[b] + BQ, BQ, sl2);
+      if (t + 2 < T) put_stat(t + 2);
       step_tail(t);
     }
     if (len % BQ) {
       const int b = t % NB;
-      if (t + 2 < T) issue((t + 2) % NB);
+      if (t + 2 < T) issue((t + 2) % NB, t + 2);
       if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], rstat[b], rstat[b] + BQ, len % BQ, sl2);
+      if (t + 2 < T) put_stat(t + 2);
       step_tail(t);
       ++t;
     }
