@@ -39,7 +39,7 @@ constexpr float kBigSum = 65536.0f;  // a lane's half-step sum of P above this f
 constexpr int kLook = 2;             // LDS fragments are read this many MFMA slots ahead
 constexpr int kWaves = kFwdQueryTile / 32;
 template <int D> using KTile = PaddedTile<D, kFwdKeyStep, kRowPadRS<D>>;  // row-fragment reads
-template <int D> using VTile = PaddedTile<D, kFwdKeyStep, kTrPadRS<D>>;   // transpose reads
+template <int D> using VTile = PaddedTile<D, kFwdKeyStep, kRowPadRS<D>>;  // transpose reads, rows permuted
 }  // namespace
 
 template <int D>
@@ -71,9 +71,10 @@ __device__ __forceinline__ bf16x8 v_frag(const __bf16* vt, int i) {
   const int lane = threadIdx.x & 63;
   const int tcol = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const int trow = 4 * (lane >> 5) + ((lane & 15) >> 2);
-  const int r0 = 16 * (i / (D / 32)) + trow, db = i % (D / 32);
-  return cat8(lds_read_tr(vt + r0 * kTrPadRS<D> + db * 32 + tcol),
-              lds_read_tr(vt + (r0 + 8) * kTrPadRS<D> + db * 32 + tcol));
+  // rows r and r + 8 of a 16-row block sit at physical rows perm16(r) and perm16(r) + 2
+  const int r0 = 16 * (i / (D / 32)) + perm16(trow), db = i % (D / 32);
+  return cat8(lds_read_tr(vt + r0 * kRowPadRS<D> + db * 32 + tcol),
+              lds_read_tr(vt + (r0 + 2) * kRowPadRS<D> + db * 32 + tcol));
 }
 
 // S^T of 32 keys, plain (used outside the pipeline).
@@ -271,7 +272,7 @@ struct FullTileCursor {
 template <int D>
 __global__ void __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
 sra_fwd_kernel(FwdArgs a) {
-  constexpr int NC = D / 16, ND = D / 32, BK = kFwdKeyStep, RK = kRowPadRS<D>, RV = kTrPadRS<D>;
+  constexpr int NC = D / 16, ND = D / 32, BK = kFwdKeyStep, RK = kRowPadRS<D>, RV = kRowPadRS<D>;
   constexpr int KE = KTile<D>::kElems, VE = VTile<D>::kElems;
   // Three buffers each for K and V, as separate arrays addressed only with compile-time
   // choices (the loop is unrolled by three): the compiler can then tell a buffer being filled
@@ -314,7 +315,7 @@ sra_fwd_kernel(FwdArgs a) {
   for (int i = 0; i < it.span_cnt; ++i) T += __builtin_amdgcn_readfirstlane(sp[i].len) / BK;
 
   TileLoader<D, BK, RK, kWaves> kl[2];
-  TileLoader<D, BK, RV, kWaves> vl[2];
+  TileLoader<D, BK, RV, kWaves, true> vl[2];  // V rows permuted in blocks of 16
 #pragma unroll
   for (int ss = 0; ss < 2; ++ss) {
     kl[ss].init(a.in_stride[ss], h, wave);
@@ -420,7 +421,7 @@ sra_fwd_kernel(FwdArgs a) {
     const int ss = __builtin_amdgcn_readfirstlane(sp_i.stream);
     const int st0 = __builtin_amdgcn_readfirstlane(sp_i.start);
     tile_load_lds<D, BK, RK, kWaves>(kbuf0, a.k[ss], a.in_stride[ss], h, st0, len, len - rem, wave);
-    tile_load_lds<D, BK, RV, kWaves>(vbuf0, a.v[ss], a.in_stride[ss], h, st0, len, len - rem, wave);
+    tile_load_lds<D, BK, RV, kWaves, true>(vbuf0, a.v[ss], a.in_stride[ss], h, st0, len, len - rem, wave);
     wait_vmem();
     __syncthreads();
     if (active) {
