@@ -31,6 +31,12 @@ __device__ __forceinline__ void mfma32_agpr(floatx16& acc, bf16x8 a, bf16x8 b) {
   asm("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
 
+// Waits out the latency of MFMAs issued by mfma32_agpr: the compiler does not see those, so
+// it inserts no wait states of its own before an accumulator is read. The kernels issue it
+// inside their step loop, after the last step, so that no accumulator read (all of which
+// follow the loop) can be scheduled above it.
+__device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory"); }
+
 __device__ __forceinline__ bf16x8 ld8(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }

@@ -269,6 +269,7 @@ sra_dkv_kernel(BwdArgs a) {
       wait_vmem();
       __syncthreads();
     }
+    if (t + 1 == T) mfma_drain();
   };
   int t = 0;
   for (int si = 0; si < it.span_cnt; ++si) {
@@ -292,9 +293,6 @@ sra_dkv_kernel(BwdArgs a) {
   }
 
   if (!active) return;
-  // the accumulators were last written by MFMAs the compiler does not see: wait out their
-  // latency before reading them
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int r = wave * 64 + 32 * j + l32;

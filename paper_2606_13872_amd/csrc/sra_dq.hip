@@ -215,6 +215,13 @@ sra_dq_kernel(BwdArgs a) {
   // Step t reads buffer t % NB and loads step t + 2 into buffer (t + 2) % NB. That buffer's
   // last reader, step t - 2, finished before the barrier ending step t - 2 or t - 1
   // (whichever is odd); the tiles of step t landed before that same barrier.
+  auto step_tail = [&](int t) {
+    if (t & 1) {
+      wait_vmem();
+      __syncthreads();
+    }
+    if (t + 1 == T) mfma_drain();
+  };
   int t = 0;
   for (int si = 0; si < it.span_cnt; ++si) {
     const int len = __builtin_amdgcn_readfirstlane(sp[si].len);
@@ -222,26 +229,17 @@ sra_dq_kernel(BwdArgs a) {
     for (int j = 0; j < full; ++j, ++t) {
       if (t + 2 < T) issue((t + 2) % NB);
       if (active) dq_step<D, false>(st, ks[t % NB], vs[t % NB], BK, sl2);
-      if (t & 1) {
-        wait_vmem();
-        __syncthreads();
-      }
+      step_tail(t);
     }
     if (len % BK) {
       if (t + 2 < T) issue((t + 2) % NB);
       if (active) dq_step<D, true>(st, ks[t % NB], vs[t % NB], len % BK, sl2);
-      if (t & 1) {
-        wait_vmem();
-        __syncthreads();
-      }
+      step_tail(t);
       ++t;
     }
   }
 
   if (!active) return;
-  // the accumulators were last written by MFMAs the compiler does not see: wait out their
-  // latency before reading them
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int r = wave * 64 + 32 * j + l32;

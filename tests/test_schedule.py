@@ -91,7 +91,8 @@ def _golden():
         return json.load(f)
 
 
-@pytest.mark.parametrize("name", ["tiny", "480p"] + [f"sweep_{n}" for n in SWEEP_POINTS] + ["720p", "varlen"])
+@pytest.mark.parametrize("name", ["tiny", "480p"] + [f"sweep_{n}" for n in SWEEP_POINTS]
+                         + ["720p", "varlen", "varlen_window", "varlen_tokens"])
 def test_full_size_pair_counts_and_coverage(name):
     w = workload(name)
     gold = _golden()[name]
