@@ -7,6 +7,7 @@ from .sra_oracle import (  # noqa: F401
     attention_backward_full,
     attention_rows,
     default_scale,
+    dkv_keys,
     dq_rows,
     forward_rows,
     frame_valid,

@@ -23,7 +23,8 @@ concatenated token order [gen ; ref] of one sample, logits S = scale * Q K^T, S 
 where M is false, a row softmax, O = P V and LSE = log sum exp(S) (natural log). The
 backward pass is the textbook gradient of that masked softmax attention. Everything is
 computed in float64 by default (float32 on request), with numpy matmul as the only
-library primitive.
+library primitive; dkv_keys, which sums over billions of (query, key) pairs at full sizes,
+runs the same formulas with torch CPU ops instead.
 
 Reading of the paper taken here (it gives no formula): reference-only attention for
 reference queries, combined with the claim of cost linear in reference length means a
@@ -292,3 +293,51 @@ def dq_rows(x, samples, b: int, h: int, rows: np.ndarray, scale=None, dtype=np.f
     D = (do * o).sum(axis=1)
     dS = P * (do @ v.T - D[:, None])
     return (dS @ k) * dtype(scale)
+
+
+def dkv_keys(x, samples, b: int, h: int, keys: np.ndarray, scale=None, dtype=np.float64,
+             block_rows: int = 4096):
+    """dK and dV of selected keys of sample b, head h (keys index [gen ; ref] of the sample).
+
+    A key's gradient sums over every query that sees it: dV_k = sum_q P_qk dO_q and
+    dK_k = scale * sum_q dS_qk Q_q, with dS_qk = P_qk (dP_qk - D_q), dP = dO V^T and
+    D = rowsum(dO * O). P_qk needs the whole softmax row of q, so every query row that sees one
+    of the keys goes through the full masked softmax; rows are taken in blocks to bound memory
+    (the sums over q are then added block by block). At full workload sizes that is billions
+    of exponentials per head, so this function does its arithmetic with torch CPU ops
+    (vectorised and multithreaded), one op per step of the formulas above; the visibility mask
+    is the same explicit one as everywhere else in this module.
+    """
+    import torch
+
+    d = x["q_gen"].shape[2]
+    scale = default_scale(d) if scale is None else scale
+    geom = samples[b]
+    tdt = torch.float64 if np.dtype(dtype) == np.float64 else torch.float32
+    cat, _, _ = _sample_head(x, samples, b, h, dtype)
+    q, do = torch.from_numpy(cat("q_gen", "q_ref")), torch.from_numpy(cat("do_gen", "do_ref"))
+    k, v = torch.from_numpy(cat("k_gen", "k_ref")), torch.from_numpy(cat("v_gen", "v_ref"))
+    keys = np.asarray(keys, dtype=np.int64)
+    kt = torch.from_numpy(keys)
+    dk = torch.zeros((len(keys), d), dtype=tdt)
+    dv = torch.zeros((len(keys), d), dtype=tdt)
+    for r0 in range(0, q.shape[0], block_rows):
+        rows = np.arange(r0, min(q.shape[0], r0 + block_rows))
+        M = visibility_mask(geom, rows)
+        sees = M[:, keys].any(axis=1)
+        if not sees.any():
+            continue
+        rows, M = torch.from_numpy(rows[sees]), torch.from_numpy(M[sees])
+        # masked softmax of the block's full rows (every row here sees at least one key)
+        S = (q[rows] @ k.T) * scale
+        S = S.masked_fill(~M, float("-inf"))
+        m = S.amax(dim=1, keepdim=True)
+        E = torch.exp(S - m)
+        P = E / E.sum(dim=1, keepdim=True)
+        o = P @ v
+        D = (do[rows] * o).sum(dim=1, keepdim=True)
+        Pk = P[:, kt]
+        dS = Pk * (do[rows] @ v[kt].T - D)
+        dv += Pk.T @ do[rows]
+        dk += (dS.T @ q[rows]) * scale
+    return dk.numpy(), dv.numpy()

@@ -5,6 +5,8 @@ The oracle cannot run whole layers at these sizes, so the checks are:
   * sampled query rows: O, LSE (forward) and dQ (backward) of chosen rows, which the oracle
     computes one by one from the full key set of each row (tile starts and ends, frame edges,
     the ragged last tile, random rows; first and last head);
+  * sampled keys: dK and dV of chosen keys, which the oracle sums over every query that sees
+    the key (each through its full softmax row);
   * the K = 0 count law on every row of every head: LSE = ln |visible keys| exactly;
   * gradient identities that hold at any size, per sample and head:
         sum over keys of dK = 0, and sum over keys of dV = sum over valid queries of dO
@@ -131,6 +133,45 @@ def test_fullsize_dq_sampled_rows(name):
         got = _gpu_rows(g["dq_gen"][:, h], g["dq_ref"][:, h], go, ro, b, geom.n_gen, rows)
         _close(f"{name} dQ b{b}", got, want)
 
+
+def _sample_keys(geom, rng, n_rand=6):
+    """Key indices into [gen ; ref] of one sample: tile edges, frame edges, the last key, random
+    keys (on a token-masked reference, some of them invalid: their gradients must be 0)."""
+    G, R, F = geom.n_gen, geom.n_ref, geom.ref_h * geom.ref_w
+    gen = {0, 1, 63, 64, 255, 256, G // 2, G - 1} | set(rng.integers(0, G, n_rand).tolist())
+    ref = set()
+    for f in sorted({0, geom.ref_frames - 1}):
+        ref |= {f * F + r for r in (0, 63, 64, 255, 256, F - 1) if 0 <= r < F}
+    ref |= set(rng.integers(0, R, n_rand).tolist())
+    return np.array(sorted(gen) + sorted(G + r for r in ref), dtype=np.int64)
+
+
+@pytest.mark.parametrize("name", ["varlen_tokens", "varlen_window"])
+def test_fullsize_dkv_sampled_keys(name):
+    """dK/dV of sampled keys against the oracle's sums over every query that sees each key (the
+    sample with the shortest reference, one head; about 10 s of oracle time per case)."""
+    w = workload(name)
+    x = _inputs(w, grads=True)
+    ins = [x[k] for k in INS]
+    o = sra.forward(*ins, w.samples)
+    g = sra.backward(*ins, *o, x["do_gen"], x["do_ref"], w.samples)
+    torch.cuda.synchronize()
+    go, ro = _offsets(w.samples)
+    b = int(np.argmin([s.n_ref for s in w.samples]))
+    geom = w.samples[b]
+    h = 1
+    keys = _sample_keys(geom, np.random.default_rng(9))
+    xh = _head_view(x, h)
+    print(f"[fullsize] {name} dK/dV head {h} sample {b}: {len(keys)} keys", flush=True)
+    want_k, want_v = oracle.dkv_keys(xh, w.samples, b, 0, keys)
+    G = geom.n_gen
+    got_k = _gpu_rows(g["dk_gen"][:, h], g["dk_ref"][:, h], go, ro, b, G, keys)
+    got_v = _gpu_rows(g["dv_gen"][:, h], g["dv_ref"][:, h], go, ro, b, G, keys)
+    dead = np.concatenate([np.zeros(int((keys < G).sum()), bool), ~_ref_token_ok(geom)[keys[keys >= G] - G]])
+    assert dead.any() == (geom.ref_token_valid is not None) and not dead.all()
+    assert np.all(got_k[dead] == 0) and np.all(got_v[dead] == 0), "invalid reference keys got gradient"
+    _close("dK", got_k[~dead], want_k[~dead])
+    _close("dV", got_v[~dead], want_v[~dead])
 
 def _ref_token_ok(geom):
     """Per reference token: its frame is valid and so is its own entry of the token mask."""

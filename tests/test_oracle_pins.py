@@ -409,6 +409,29 @@ def test_row_block_mode_matches_full():
             assert (np.isneginf(ref_l) and np.isneginf(lse[i])) or abs(lse[i] - ref_l) < 1e-12
 
 
+def test_key_block_mode_matches_full():
+    """dK/dV of sampled keys (full softmax rows in blocks) equal the full backward's columns."""
+    rng = np.random.default_rng(31)
+    tok = (rng.random(3 * 16) < 0.7).astype(np.uint8).tolist()
+    samples = [SampleGeom(3, 4, 4, 3, 4, 4, frame_valid=[1, 0, 1], ref_token_valid=tok),
+               SampleGeom(4, 2, 4, 2, 4, 4, gen_window=1),
+               SampleGeom(2, 4, 4, 3, 4, 4, group_frames=2)]
+    x = rand_inputs(samples, 2, 8, grads=True)
+    g = oracle.sra_backward(x, samples)
+    go, ro = [0, 48, 80], [0, 48, 80]
+    for b, geom in enumerate(samples):
+        G, R = geom.n_gen, geom.n_ref
+        keys = np.array(sorted(set(rng.integers(0, G + R, 12).tolist()) | {0, G - 1, G, G + R - 1}))
+        for block in (5, 64):
+            dk, dv = oracle.dkv_keys(x, samples, b, 1, keys, block_rows=block)
+            for i, kk in enumerate(keys):
+                if kk < G:
+                    want_k, want_v = g["dk_gen"][go[b] + kk, 1], g["dv_gen"][go[b] + kk, 1]
+                else:
+                    want_k, want_v = g["dk_ref"][ro[b] + kk - G, 1], g["dv_ref"][ro[b] + kk - G, 1]
+                np.testing.assert_allclose(dk[i], want_k, rtol=1e-10, atol=1e-13)
+                np.testing.assert_allclose(dv[i], want_v, rtol=1e-10, atol=1e-13)
+
 def test_varlen_samples_do_not_interact():
     samples = [SampleGeom(1, 2, 4, 2, 2, 4), SampleGeom(2, 2, 2, 1, 2, 4)]
     x = rand_inputs(samples, 1, 8, grads=True)
