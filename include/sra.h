@@ -156,7 +156,12 @@ sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, ui
 /* Copies schedule `which` into host buffers: items[8*i + 0..7] = {stream, head, start, length,
  * span_offset, span_count, sample, reserved} per work item, spans[4*j + 0..3] = {stream,
  * start, length, reserved} per span (stream 0 = gen, 1 = ref; start = packed token row).
- * items/spans may be NULL to query only; capacities count int32 elements. */
+ * items/spans may be NULL to query only; capacities count int32 elements.
+ * When token masks split reference frames into more runs of valid tokens than there are
+ * groups with a valid token, the library runs on the compacted reference stream (the valid
+ * reference tokens of the batch back to back, in sample, group and token order: gathered
+ * before the kernels, outputs scattered back after); ref rows of the schedule are then rows
+ * of that stream. */
 sra_status sra_schedule_export(const sra_problem* p, int which, int32_t* items,
                                int64_t items_capacity, int32_t* spans, int64_t spans_capacity);
 
@@ -169,7 +174,9 @@ enum {
   SRA_KERNEL_DKDV = 2,      /* backward: dK and dV (key-major)           */
   SRA_KERNEL_DQ = 3,        /* backward: dQ (query-major)                */
   SRA_KERNEL_FILL = 4,      /* rows of invalid reference frames          */
-  SRA_KERNEL_COUNT = 5
+  SRA_KERNEL_GATHER = 5,    /* reference rows into the compacted stream  */
+  SRA_KERNEL_SCATTER = 6,   /* compacted rows back to the reference rows */
+  SRA_KERNEL_COUNT = 7
 };
 
 /* enable != 0: from now on every kernel launch is bracketed by two hipEvents recorded on the

@@ -38,6 +38,7 @@ std::vector<RowRun> valid_runs(const SampleLayout& s, int64_t lo, int64_t hi) {
 
 // Rows of ref group g0 (its first frame) of a sample.
 RowRun group_rows(const SampleLayout& s, int32_t g0) {
+  if (!s.gbound.empty()) return {s.gbound[g0 / s.group], s.gbound[g0 / s.group + 1]};
   return {int64_t(g0) * s.F, int64_t(std::min(s.ref_frames, g0 + s.group)) * s.F};
 }
 
@@ -305,8 +306,55 @@ void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
 
 }  // namespace
 
-void build_plan(const Layout& L, Plan* plan) {
-  plan->layout = L;
+bool needs_compaction(const Layout& L) {
+  for (const SampleLayout& s : L.samples) {
+    int64_t groups = 0;
+    for (int32_t g0 = 0; g0 < s.ref_frames; g0 += s.group) {
+      const RowRun gr = group_rows(s, g0);
+      if (!valid_runs(s, gr.r0, gr.r1).empty()) ++groups;
+    }
+    if (int64_t(s.vruns.size()) > groups) return true;
+  }
+  return false;
+}
+
+void compact_layout(const Layout& L, Layout* C, std::vector<int32_t>* gather, std::vector<int32_t>* scatter) {
+  *C = L;
+  C->sum_ref = 0;
+  gather->clear();
+  scatter->assign(size_t(L.sum_ref), -1);
+  for (size_t b = 0; b < L.samples.size(); ++b) {
+    const SampleLayout& s = L.samples[b];
+    SampleLayout& c = C->samples[b];
+    c.ref_off = C->sum_ref;
+    c.gbound.assign(1, 0);
+    int64_t n = 0;
+    for (int32_t g0 = 0; g0 < s.ref_frames; g0 += s.group) {
+      const RowRun gr = group_rows(s, g0);
+      for (const RowRun& r : valid_runs(s, gr.r0, gr.r1))
+        for (int64_t row = r.r0; row < r.r1; ++row, ++n) {
+          (*scatter)[size_t(s.ref_off + row)] = int32_t(c.ref_off + n);
+          gather->push_back(int32_t(s.ref_off + row));
+        }
+      c.gbound.push_back(n);
+    }
+    c.R = n;
+    c.vruns.clear();
+    if (n > 0) c.vruns.push_back({0, n});
+    C->sum_ref += n;
+  }
+}
+
+void build_plan(const Layout& L_in, Plan* plan) {
+  plan->layout = L_in;
+  plan->compacted = needs_compaction(L_in);
+  plan->ref_gather.clear();
+  plan->ref_scatter.clear();
+  if (plan->compacted)
+    compact_layout(L_in, &plan->exec, &plan->ref_gather, &plan->ref_scatter);
+  else
+    plan->exec = L_in;
+  const Layout& L = plan->exec;
   build_query_major(L, kFwdQueryTile, kFwdKeyStep, &plan->fwd);
   build_query_major(L, kDqQueryTile, kDqKeyStep, &plan->dq);
   build_key_major(L, kDkvKeyTile, kDkvQueryStep, &plan->dkv);

@@ -22,6 +22,9 @@ struct SampleLayout {
   // maximal runs [first, last) of valid ref token rows (sample-relative): a token is valid when
   // its frame is and, with a token mask, its own entry is
   std::vector<std::pair<int64_t, int64_t>> vruns;
+  // Row bounds of the ref groups when they are not runs of F-row frames (the compacted
+  // reference stream, below): group i holds rows [gbound[i], gbound[i + 1]). Empty otherwise.
+  std::vector<int64_t> gbound;
 };
 
 struct Layout {
@@ -40,10 +43,19 @@ struct Schedule {
   int64_t real_items = 0;
 };
 
+// When a token mask splits reference frames into many short runs of valid tokens, tiles cut
+// per run would be mostly empty. Such a plan runs on the compacted reference stream instead:
+// the valid ref tokens of the batch gathered back to back (sample-major, then group-major,
+// keeping their order), so every group is one contiguous run. The library gathers the
+// reference inputs into that stream before the kernels and scatters the outputs back after.
 struct Plan {
-  Layout layout;
+  Layout layout;                   // as given
+  bool compacted = false;          // the schedules index the compacted reference stream
+  Layout exec;                     // the layout the schedules index (layout, or its compaction)
   Schedule fwd, dq, dkv;
-  std::vector<FillRange> fill;   // invalid reference rows
+  std::vector<FillRange> fill;     // invalid reference rows of exec (none when compacted)
+  std::vector<int32_t> ref_gather;   // compacted: packed ref row of each compacted row
+  std::vector<int32_t> ref_scatter;  // compacted: compacted row of each packed ref row, or -1
 };
 
 // Validates `p` and derives the layout. Returns SRA_OK or an error with `err` set.
@@ -52,7 +64,15 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err);
 // Closed-form visible pairs per head (summed over samples).
 void closed_form_pairs(const Layout& L, int64_t* gen_pairs, int64_t* ref_pairs);
 
-// Builds the three schedules and the fill list.
+// True when some sample's token mask splits its reference frames into more runs of valid
+// tokens than it has groups with a valid token (frame masks alone never do).
+bool needs_compaction(const Layout& L);
+
+// The compacted form of L (every sample's valid ref tokens back to back, groups given by
+// gbound) with the row maps between the two reference streams.
+void compact_layout(const Layout& L, Layout* C, std::vector<int32_t>* gather, std::vector<int32_t>* scatter);
+
+// Builds the three schedules and the fill list (on the compacted layout when needed).
 void build_plan(const Layout& L, Plan* plan);
 
 // Pairs per head covered by a schedule (head 0 items only, so per head).

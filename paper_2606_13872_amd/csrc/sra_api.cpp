@@ -39,8 +39,8 @@ struct Blob {
 
 struct CachedPlan {
   Plan plan;
-  Blob fwd;   // fwd items | fwd spans | fill
-  Blob bwd;   // dq items | dq spans | dkv items | dkv spans | fill
+  Blob fwd;   // fwd items | fwd spans | fill | ref gather | ref scatter
+  Blob bwd;   // dq items | dq spans | dkv items | dkv spans | fill | ref gather | ref scatter
   // Runs when the cache has dropped the plan and no call holds it any more. An upload
   // enqueued by an earlier call may still read the pinned images: wait for the device.
   ~CachedPlan() {
@@ -76,11 +76,15 @@ class PlanCache {
     put_table(cp->fwd, cp->plan.fwd.items);
     put_table(cp->fwd, cp->plan.fwd.spans);
     put_table(cp->fwd, cp->plan.fill);
+    put_table(cp->fwd, cp->plan.ref_gather);
+    put_table(cp->fwd, cp->plan.ref_scatter);
     put_table(cp->bwd, cp->plan.dq.items);
     put_table(cp->bwd, cp->plan.dq.spans);
     put_table(cp->bwd, cp->plan.dkv.items);
     put_table(cp->bwd, cp->plan.dkv.spans);
     put_table(cp->bwd, cp->plan.fill);
+    put_table(cp->bwd, cp->plan.ref_gather);
+    put_table(cp->bwd, cp->plan.ref_scatter);
     if (map_.size() >= kMaxPlans) evict_one();
     lru_.push_front(key);
     map_[key] = {cp, lru_.begin()};
@@ -128,12 +132,23 @@ PlanCache& cache() {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
-size_t fwd_workspace(const CachedPlan& cp) { return cp.fwd.bytes; }
-size_t bwd_workspace(const CachedPlan& cp, const Layout& L) {
-  // schedule, then -D and the LSE in log2 units per query row of each stream
-  size_t b = cp.bwd.bytes;
-  b += 2 * align_up(size_t(L.heads) * L.sum_gen * sizeof(float));
-  b += 2 * align_up(size_t(L.heads) * L.sum_ref * sizeof(float));
+// Bytes of `rows` dense bf16 rows of all heads, and of one fp32 value per (head, row).
+size_t rows_bytes(const Layout& L, int64_t rows) { return align_up(size_t(rows) * L.heads * L.head_dim * 2); }
+size_t stat_bytes(const Layout& L, int64_t rows) { return align_up(size_t(L.heads) * rows * sizeof(float)); }
+
+// Forward workspace: schedule, then (compacted plans) the compacted ref q, k, v, o and lse.
+size_t fwd_workspace(const CachedPlan& cp) {
+  const Layout& E = cp.plan.exec;
+  size_t b = cp.fwd.bytes;
+  if (cp.plan.compacted) b += 4 * rows_bytes(E, E.sum_ref) + stat_bytes(E, E.sum_ref);
+  return b;
+}
+// Backward workspace: schedule; -D and the LSE in log2 units per query row of each stream;
+// then (compacted plans) the compacted ref q, k, v, o, do, dq, dk, dv and lse.
+size_t bwd_workspace(const CachedPlan& cp) {
+  const Layout& E = cp.plan.exec;
+  size_t b = cp.bwd.bytes + 2 * stat_bytes(E, E.sum_gen) + 2 * stat_bytes(E, E.sum_ref);
+  if (cp.plan.compacted) b += 8 * rows_bytes(E, E.sum_ref) + stat_bytes(E, E.sum_ref);
   return b;
 }
 
@@ -255,7 +270,7 @@ sra_status sra_workspace_size(const sra_problem* p, int backward, size_t* bytes)
   std::shared_ptr<CachedPlan> cp;
   sra_status st = common_checks(p, &L, &cp);
   if (st != SRA_OK) return st;
-  *bytes = backward ? bwd_workspace(*cp, L) : fwd_workspace(*cp);
+  *bytes = backward ? bwd_workspace(*cp) : fwd_workspace(*cp);
   return SRA_OK;
 }
 
@@ -287,6 +302,8 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
     if (e != hipSuccess) return hip_fail(e, "schedule upload");
   }
   const Plan& P = cp->plan;
+  const Layout& E = P.exec;
+  const int32_t row_elems = L.heads * L.head_dim;
   FwdArgs a{};
   a.items = reinterpret_cast<const WorkItem*>(ws + cp->fwd.offsets[0]);
   a.spans = reinterpret_cast<const Span*>(ws + cp->fwd.offsets[1]);
@@ -303,11 +320,56 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
   a.lse[0] = lse_gen;
   a.lse[1] = lse_ref;
   a.rows[0] = int32_t(L.sum_gen);
-  a.rows[1] = int32_t(L.sum_ref);
+  a.rows[1] = int32_t(E.sum_ref);
   a.heads = L.heads;
   a.scale_log2 = float(double(L.scale) * 1.4426950408889634);
-  hipError_t e = timed(SRA_KERNEL_FORWARD, s, [&] { return launch_forward(a, int(P.fwd.items.size()), L.head_dim, s); });
+  hipError_t e;
+  __bf16* o_c = nullptr;
+  float* lse_c = nullptr;
+  if (P.compacted) {  // the kernels read and write the compacted reference stream
+    char* c = ws + cp->fwd.bytes;
+    const size_t rb = rows_bytes(E, E.sum_ref);
+    __bf16* qkv_c[3] = {reinterpret_cast<__bf16*>(c), reinterpret_cast<__bf16*>(c + rb),
+                        reinterpret_cast<__bf16*>(c + 2 * rb)};
+    o_c = reinterpret_cast<__bf16*>(c + 3 * rb);
+    lse_c = reinterpret_cast<float*>(c + 4 * rb);
+    GatherArgs g{};
+    g.index = reinterpret_cast<const int32_t*>(ws + cp->fwd.offsets[3]);
+    g.rows = int32_t(E.sum_ref);
+    g.row_elems = row_elems;
+    g.heads = L.heads;
+    g.src[0] = L.gen_only ? nullptr : a.q[1];  // no reference queries when gen-only
+    g.src[1] = a.k[1];
+    g.src[2] = a.v[1];
+    for (int t = 0; t < 3; ++t) {
+      g.src_stride[t] = L.ref_stride;
+      g.dst[t] = qkv_c[t];
+    }
+    e = timed(SRA_KERNEL_GATHER, s, [&] { return launch_gather(g, s); });
+    if (e != hipSuccess) return hip_fail(e, "gather launch");
+    a.q[1] = L.gen_only ? nullptr : qkv_c[0];
+    a.k[1] = qkv_c[1];
+    a.v[1] = qkv_c[2];
+    a.in_stride[1] = row_elems;
+    a.o[1] = o_c;
+    a.lse[1] = lse_c;
+  }
+  e = timed(SRA_KERNEL_FORWARD, s, [&] { return launch_forward(a, int(P.fwd.items.size()), L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "forward launch");
+  if (P.compacted && !L.gen_only) {
+    ScatterArgs sc{};
+    sc.index = reinterpret_cast<const int32_t*>(ws + cp->fwd.offsets[4]);
+    sc.rows = int32_t(L.sum_ref);
+    sc.row_elems = row_elems;
+    sc.heads = L.heads;
+    sc.src[0] = o_c;
+    sc.dst[0] = static_cast<__bf16*>(o_ref);
+    sc.lse_src = lse_c;
+    sc.lse_src_rows = int32_t(E.sum_ref);
+    sc.lse_dst = lse_ref;
+    e = timed(SRA_KERNEL_SCATTER, s, [&] { return launch_scatter(sc, s); });
+    if (e != hipSuccess) return hip_fail(e, "scatter launch");
+  }
   if (!P.fill.empty() && !L.gen_only) {  // ref rows of invalid frames (no ref rows when gen-only)
     FillArgs f{};
     f.ranges = reinterpret_cast<const FillRange*>(ws + cp->fwd.offsets[2]);
@@ -338,7 +400,7 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
                   : check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen, do_gen, dq_gen, dk_gen, dv_gen},
                                   {q_ref, k_ref, v_ref, o_ref, lse_ref, do_ref, dq_ref, dk_ref, dv_ref});
   if (st != SRA_OK) return st;
-  const size_t need = bwd_workspace(*cp, L);
+  const size_t need = bwd_workspace(*cp);
   if (workspace_bytes < need)
     return fail(SRA_ERR_WORKSPACE_TOO_SMALL, "backward needs " + std::to_string(need) + " workspace bytes");
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign))
@@ -351,42 +413,80 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
   if (st != SRA_OK) return st;
   hipError_t e = hipMemcpyAsync(ws, src, cp->bwd.bytes, hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "schedule upload");
-  const size_t gen_stat = align_up(size_t(L.heads) * L.sum_gen * sizeof(float));
-  const size_t ref_stat = align_up(size_t(L.heads) * L.sum_ref * sizeof(float));
+  const Plan& P = cp->plan;
+  const Layout& E = P.exec;
+  const int32_t row_elems = L.heads * L.head_dim;
+  const size_t gen_stat = stat_bytes(E, E.sum_gen);
+  const size_t ref_stat = stat_bytes(E, E.sum_ref);
   float* ndelta_gen = reinterpret_cast<float*>(ws + cp->bwd.bytes);
   float* lse2_gen = reinterpret_cast<float*>(ws + cp->bwd.bytes + gen_stat);
   float* ndelta_ref = reinterpret_cast<float*>(ws + cp->bwd.bytes + 2 * gen_stat);
   float* lse2_ref = reinterpret_cast<float*>(ws + cp->bwd.bytes + 2 * gen_stat + ref_stat);
 
+  // the reference tensors the kernels use: the caller's, or their compacted copies
+  const __bf16* ref_in[5] = {static_cast<const __bf16*>(q_ref), static_cast<const __bf16*>(k_ref),
+                             static_cast<const __bf16*>(v_ref), static_cast<const __bf16*>(o_ref),
+                             static_cast<const __bf16*>(do_ref)};
+  __bf16* ref_out[3] = {static_cast<__bf16*>(dq_ref), static_cast<__bf16*>(dk_ref), static_cast<__bf16*>(dv_ref)};
+  const float* ref_lse = lse_ref;
+  int64_t ref_stride = L.ref_stride;
+  if (P.compacted) {
+    char* c = ws + cp->bwd.bytes + 2 * gen_stat + 2 * ref_stat;
+    const size_t rb = rows_bytes(E, E.sum_ref);
+    GatherArgs g{};
+    g.index = reinterpret_cast<const int32_t*>(ws + cp->bwd.offsets[5]);
+    g.rows = int32_t(E.sum_ref);
+    g.row_elems = row_elems;
+    g.heads = L.heads;
+    for (int t = 0; t < 5; ++t) {
+      // q, o and do of the reference rows are not read when reference tokens are not queries
+      const bool used = !(L.gen_only && (t == 0 || t == 3 || t == 4));
+      g.src[t] = used ? ref_in[t] : nullptr;
+      g.src_stride[t] = t < 3 ? L.ref_stride : row_elems;
+      g.dst[t] = reinterpret_cast<__bf16*>(c + t * rb);
+      ref_in[t] = used ? g.dst[t] : nullptr;
+    }
+    float* lse_c = reinterpret_cast<float*>(c + 8 * rb);
+    if (!L.gen_only) {
+      g.lse_src = lse_ref;
+      g.lse_src_rows = int32_t(L.sum_ref);
+      g.lse_dst = lse_c;
+    }
+    e = timed(SRA_KERNEL_GATHER, s, [&] { return launch_gather(g, s); });
+    if (e != hipSuccess) return hip_fail(e, "gather launch");
+    for (int t = 0; t < 3; ++t) ref_out[t] = reinterpret_cast<__bf16*>(c + (5 + t) * rb);
+    ref_lse = L.gen_only ? nullptr : lse_c;
+    ref_stride = row_elems;
+  }
+
   DeltaArgs d{};
   d.o[0] = static_cast<const __bf16*>(o_gen);
-  d.o[1] = static_cast<const __bf16*>(o_ref);
+  d.o[1] = ref_in[3];
   d.dout[0] = static_cast<const __bf16*>(do_gen);
-  d.dout[1] = static_cast<const __bf16*>(do_ref);
+  d.dout[1] = ref_in[4];
   d.lse[0] = lse_gen;
-  d.lse[1] = lse_ref;
+  d.lse[1] = ref_lse;
   d.ndelta[0] = ndelta_gen;
   d.ndelta[1] = ndelta_ref;
   d.lse2[0] = lse2_gen;
   d.lse2[1] = lse2_ref;
-  d.rows[0] = int32_t(L.sum_gen);
-  d.rows[1] = L.gen_only ? 0 : int32_t(L.sum_ref);  // no ref query rows when gen-only
+  d.rows[0] = int32_t(E.sum_gen);
+  d.rows[1] = L.gen_only ? 0 : int32_t(E.sum_ref);  // no ref query rows when gen-only
   d.heads = L.heads;
   e = timed(SRA_KERNEL_DELTA, s, [&] { return launch_delta(d, L.head_dim, s); });
   if (e != hipSuccess) return hip_fail(e, "delta launch");
 
-  const Plan& P = cp->plan;
   BwdArgs a{};
   a.q[0] = static_cast<const __bf16*>(q_gen);
   a.k[0] = static_cast<const __bf16*>(k_gen);
   a.v[0] = static_cast<const __bf16*>(v_gen);
-  a.q[1] = static_cast<const __bf16*>(q_ref);
-  a.k[1] = static_cast<const __bf16*>(k_ref);
-  a.v[1] = static_cast<const __bf16*>(v_ref);
+  a.q[1] = ref_in[0];
+  a.k[1] = ref_in[1];
+  a.v[1] = ref_in[2];
   a.in_stride[0] = L.gen_stride;
-  a.in_stride[1] = L.ref_stride;
+  a.in_stride[1] = ref_stride;
   a.dout[0] = static_cast<const __bf16*>(do_gen);
-  a.dout[1] = static_cast<const __bf16*>(do_ref);
+  a.dout[1] = ref_in[4];
   a.lse2[0] = lse2_gen;
   a.lse2[1] = lse2_ref;
   a.ndelta[0] = ndelta_gen;
@@ -394,11 +494,11 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
   a.dq[0] = static_cast<__bf16*>(dq_gen);
   a.dk[0] = static_cast<__bf16*>(dk_gen);
   a.dv[0] = static_cast<__bf16*>(dv_gen);
-  a.dq[1] = static_cast<__bf16*>(dq_ref);
-  a.dk[1] = static_cast<__bf16*>(dk_ref);
-  a.dv[1] = static_cast<__bf16*>(dv_ref);
-  a.rows[0] = int32_t(L.sum_gen);
-  a.rows[1] = int32_t(L.sum_ref);
+  a.dq[1] = ref_out[0];
+  a.dk[1] = ref_out[1];
+  a.dv[1] = ref_out[2];
+  a.rows[0] = int32_t(E.sum_gen);
+  a.rows[1] = int32_t(E.sum_ref);
   a.heads = L.heads;
   a.scale = L.scale;
   a.scale_log2 = float(double(L.scale) * 1.4426950408889634);
@@ -417,11 +517,24 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
     f.n_ranges = int32_t(P.fill.size());
     f.heads = L.heads;
     f.head_dim = L.head_dim;
-    f.t[0] = L.gen_only ? nullptr : static_cast<__bf16*>(dq_ref);
-    f.t[1] = static_cast<__bf16*>(dk_ref);
-    f.t[2] = static_cast<__bf16*>(dv_ref);
+    f.t[0] = L.gen_only ? nullptr : ref_out[0];
+    f.t[1] = ref_out[1];
+    f.t[2] = ref_out[2];
     e = timed(SRA_KERNEL_FILL, s, [&] { return launch_fill(f, s); });
     if (e != hipSuccess) return hip_fail(e, "fill launch");
+  }
+  if (P.compacted) {
+    ScatterArgs sc{};
+    sc.index = reinterpret_cast<const int32_t*>(ws + cp->bwd.offsets[6]);
+    sc.rows = int32_t(L.sum_ref);
+    sc.row_elems = row_elems;
+    sc.heads = L.heads;
+    for (int t = 0; t < 3; ++t) sc.src[t] = ref_out[t];
+    sc.dst[0] = L.gen_only ? nullptr : static_cast<__bf16*>(dq_ref);
+    sc.dst[1] = static_cast<__bf16*>(dk_ref);
+    sc.dst[2] = static_cast<__bf16*>(dv_ref);
+    e = timed(SRA_KERNEL_SCATTER, s, [&] { return launch_scatter(sc, s); });
+    if (e != hipSuccess) return hip_fail(e, "scatter launch");
   }
   return SRA_OK;
 }
@@ -478,7 +591,12 @@ sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, ui
   const int64_t n = sm.G + sm.R;
   std::memset(out, 0, size_t(n * n));
   auto local = [&](int32_t stream, int64_t row) -> int64_t {  // packed row -> [gen ; ref] index
-    return stream == 0 ? row - sm.gen_off : sm.G + (row - sm.ref_off);
+    if (stream == 0) return row - sm.gen_off;
+    if (P.compacted) {  // a row of the compacted reference stream: map it back
+      if (row < 0 || row >= int64_t(P.ref_gather.size())) return -1;
+      row = P.ref_gather[size_t(row)];
+    }
+    return sm.G + (row - sm.ref_off);
   };
   const bool key_major = which == SRA_SCHED_BWD_DKDV;
   for (const WorkItem& w : S->items) {

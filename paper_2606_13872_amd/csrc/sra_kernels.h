@@ -61,10 +61,41 @@ struct FillArgs {
   int32_t lse_rows;
 };
 
+// Reference rows into the compacted stream (token masks that split frames).
+constexpr int kGatherMax = 5;
+struct GatherArgs {
+  const int32_t* index;          // [rows]: packed ref row of each compacted row
+  int32_t rows;                  // compacted rows
+  int32_t row_elems;             // heads * D
+  const __bf16* src[kGatherMax]; // [packed rows] tensors with token strides src_stride (may be null)
+  int64_t src_stride[kGatherMax];
+  __bf16* dst[kGatherMax];       // dense [rows, heads, D]
+  const float* lse_src;          // [heads, lse_src_rows] (may be null)
+  int32_t lse_src_rows;
+  float* lse_dst;                // [heads, rows]
+  int32_t heads;
+};
+
+// Compacted rows back to the packed reference stream; invalid rows get 0 (and -inf LSE).
+constexpr int kScatterMax = 3;
+struct ScatterArgs {
+  const int32_t* index;           // [rows]: compacted row of each packed ref row, -1 = invalid
+  int32_t rows;                   // packed ref rows
+  int32_t row_elems;              // heads * D
+  const __bf16* src[kScatterMax]; // dense [compacted rows, heads, D]
+  __bf16* dst[kScatterMax];       // dense [rows, heads, D] (may be null)
+  const float* lse_src;           // [heads, lse_src_rows] compacted
+  int32_t lse_src_rows;
+  float* lse_dst;                 // [heads, rows] (may be null)
+  int32_t heads;
+};
+
 hipError_t launch_forward(const FwdArgs& a, int n_items, int head_dim, hipStream_t stream);
 hipError_t launch_delta(const DeltaArgs& a, int head_dim, hipStream_t stream);
 hipError_t launch_dq(const BwdArgs& a, int n_items, int head_dim, hipStream_t stream);
 hipError_t launch_dkv(const BwdArgs& a, int n_items, int head_dim, hipStream_t stream);
 hipError_t launch_fill(const FillArgs& a, hipStream_t stream);
+hipError_t launch_gather(const GatherArgs& a, hipStream_t stream);
+hipError_t launch_scatter(const ScatterArgs& a, hipStream_t stream);
 
 }  // namespace sra

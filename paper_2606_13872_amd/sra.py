@@ -201,7 +201,7 @@ def release_caches() -> None:
     _check(lib().sra_release_caches())
 
 
-KERNELS = {"forward": 0, "delta": 1, "dkdv": 2, "dq": 3, "fill": 4}
+KERNELS = {"forward": 0, "delta": 1, "dkdv": 2, "dq": 3, "fill": 4, "gather": 5, "scatter": 6}
 
 
 def kernel_timing_enable(on: bool = True) -> None:

@@ -157,9 +157,17 @@ def test_fp32_oracle_meets_the_same_bar():
         assert_close(n, got[n], w[n].astype(np.float64), 1)
 
 
-def test_strided_qkv_packed_inputs():
+STRIDED_CASES = {
+    "frames": [SampleGeom(2, 10, 12, 3, 7, 9)],
+    # a token mask that splits frames: the reference rows are gathered from the strided views
+    "tokens": [SampleGeom(2, 10, 12, 3, 7, 9, ref_token_valid=_rand_tokens(189, 47, 0.3))],
+}
+
+
+@pytest.mark.parametrize("case", list(STRIDED_CASES))
+def test_strided_qkv_packed_inputs(case):
     """q, k, v as views of one [tokens, 3, H, d] buffer (token stride 3*H*d)."""
-    samples, H, d = [SampleGeom(2, 10, 12, 3, 7, 9)], 2, 128
+    samples, H, d = STRIDED_CASES[case], 2, 128
     x = make_inputs(samples, H, d, 23)
     dev = torch.device("cuda")
     packed = {}
@@ -227,9 +235,16 @@ def test_run_to_run_determinism():
         assert torch.equal(a[n], b[n]), n
 
 
-def test_canary_guard_bands_untouched():
+CANARY_CASES = {
+    "frames": [SampleGeom(1, 20, 13, 3, 11, 7, frame_valid=[1, 0, 1])],
+    "tokens": [SampleGeom(1, 20, 13, 3, 11, 7, frame_valid=[1, 0, 1], ref_token_valid=_rand_tokens(231, 48, 0.3))],
+}
+
+
+@pytest.mark.parametrize("case", list(CANARY_CASES))
+def test_canary_guard_bands_untouched(case):
     """Outputs live inside larger buffers filled with a sentinel; nothing outside is written."""
-    samples, H, d = [SampleGeom(1, 20, 13, 3, 11, 7, frame_valid=[1, 0, 1])], 2, 128
+    samples, H, d = CANARY_CASES[case], 2, 128
     x = make_inputs(samples, H, d, 27)
     dev = torch.device("cuda")
     y = {k: v.to(dev) for k, v in x.items()}
@@ -295,6 +310,8 @@ def test_error_paths_do_not_launch():
 GEN_ONLY_CASES = {
     "invalid_groups": [SampleGeom(2, 12, 13, 6, 5, 7, group_frames=2, frame_valid=[1, 0, 1, 1, 0, 0])],
     "varlen": [SampleGeom(2, 9, 15, 2, 9, 15), SampleGeom(1, 11, 7, 5, 6, 6), SampleGeom(1, 5, 5, 0, 3, 3)],
+    "tokens": [SampleGeom(2, 9, 15, 3, 9, 15, frame_valid=[1, 0, 1], ref_token_valid=_rand_tokens(405, 49, 0.3)),
+               SampleGeom(1, 11, 7, 2, 6, 6)],
 }
 
 

@@ -151,3 +151,29 @@ def test_xcd_order_pins_heads_and_puts_long_items_first():
         assert np.all(sub[:, 1] % 8 == x)
         cost = np.array([spans[i[4]:i[4] + i[5], 2].sum() for i in sub])
         assert np.all(np.diff(cost) <= 0)
+
+
+def test_token_masks_that_split_frames_run_on_the_compacted_stream():
+    """A token mask that splits frames into runs: the gen queries of each sample see its valid
+    reference tokens as one span of the compacted stream (the valid tokens of the batch back
+    to back). A mask that removes only whole frames keeps the frame runs of the packed stream."""
+    F = 6 * 7
+    tok = (np.random.default_rng(5).random(3 * F) >= 0.3).astype(np.uint8)
+    split = [SampleGeom(2, 5, 6, 3, 6, 7, ref_token_valid=tuple(tok.tolist())), SampleGeom(1, 4, 4, 2, 6, 7)]
+    n_valid = [int(tok.sum()), 2 * F]
+    items, spans = sra.schedule_export(split, sra.SCHED_FORWARD)
+    for b in range(2):
+        it = items[(items[:, 0] == 0) & (items[:, 6] == b)][0]
+        own = spans[it[4]:it[4] + it[5]]
+        ref = own[own[:, 0] == 1]
+        assert len(ref) == 1 and ref[0, 2] == n_valid[b] and ref[0, 1] == sum(n_valid[:b])
+    # every compacted reference row is covered once per head by the reference query tiles
+    cov = np.zeros(sum(n_valid), dtype=np.int32)
+    for it in items[(items[:, 0] == 1) & (items[:, 1] == 0)]:
+        cov[it[2]:it[2] + it[3]] += 1
+    assert np.all(cov == 1)
+    whole = [SampleGeom(2, 5, 6, 3, 6, 7, ref_token_valid=tuple([1] * F + [0] * F + [1] * F))]
+    items, spans = sra.schedule_export(whole, sra.SCHED_FORWARD)
+    it = items[items[:, 0] == 0][0]
+    own = spans[it[4]:it[4] + it[5]]
+    assert [tuple(r[1:3]) for r in own[own[:, 0] == 1]] == [(0, F), (2 * F, F)]
