@@ -140,46 +140,58 @@ def _workload_config(w):
     }
 
 
+def _fit(xs, ys):
+    """Least-squares line ys ~ icpt + slope * xs, with R^2."""
+    n = len(xs)
+    mx, my = sum(xs) / n, sum(ys) / n
+    sxx = sum((x - mx) ** 2 for x in xs)
+    slope = sum((x - mx) * (y - my) for x, y in zip(xs, ys)) / sxx
+    icpt = my - slope * mx
+    ss_res = sum((y - (icpt + slope * x)) ** 2 for x, y in zip(xs, ys))
+    ss_tot = sum((y - my) ** 2 for y in ys)
+    return {"slope_ms_per_1k_tokens": round(slope * 1000, 5), "intercept_ms": round(icpt, 4),
+            "r2": round(1 - ss_res / ss_tot, 6) if ss_tot > 0 else 1.0}
+
+
 def _sweep(sra, torch, reps):
     from sra_inputs import SWEEP_POINTS, make_inputs, workload
 
-    rs, ms, pairs = [], [], []
-    for n in SWEEP_POINTS:
-        w = workload(f"sweep_{n}")
-        x = make_inputs(w.samples, w.heads, w.head_dim, w.seed, w.rms_norm_qk, device="cuda", grads=False)
-        out = {}
-        args = [x[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
-        o = sra.forward(*args, w.samples)
-        out = {"o_gen": o[0], "o_ref": o[1], "lse_gen": o[2], "lse_ref": o[3]}
-        torch.cuda.synchronize()
+    def timed(fn):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
         for _ in range(reps):
-            sra.forward(*args, w.samples, out=out)
+            fn()
         e1.record()
         torch.cuda.synchronize()
-        rs.append(sum(g.n_ref for g in w.samples))
-        ms.append(e0.elapsed_time(e1) / reps)
+        return e0.elapsed_time(e1) / reps
+
+    rs, ms, ms_b, pairs = [], [], [], []
+    for n in SWEEP_POINTS:
+        w = workload(f"sweep_{n}")
+        x = make_inputs(w.samples, w.heads, w.head_dim, w.seed, w.rms_norm_qk, device="cuda", grads=True)
+        args = [x[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
+        o = sra.forward(*args, w.samples)
+        out = {"o_gen": o[0], "o_ref": o[1], "lse_gen": o[2], "lse_ref": o[3]}
+        g = sra.backward(*args, *o, x["do_gen"], x["do_ref"], w.samples)
+        torch.cuda.synchronize()
+        ms.append(timed(lambda: sra.forward(*args, w.samples, out=out)))
+        ms_b.append(timed(lambda: sra.backward(*args, *o, x["do_gen"], x["do_ref"], w.samples, out=g)))
+        rs.append(sum(s.n_ref for s in w.samples))
         gp, rp = sra.pair_counts(w.samples, w.heads, w.head_dim)
         pairs.append(gp + rp)
-        del x, out, args, o
+        del x, out, args, o, g
         torch.cuda.empty_cache()
-        print(f"[bench] sweep R={rs[-1]} fwd {ms[-1]:.2f} ms", file=sys.stderr, flush=True)
-    n = len(rs)
-    mr, mm = sum(rs) / n, sum(ms) / n
-    sxx = sum((r - mr) ** 2 for r in rs)
-    slope = sum((r - mr) * (m - mm) for r, m in zip(rs, ms)) / sxx
-    icpt = mm - slope * mr
-    ss_res = sum((m - (icpt + slope * r)) ** 2 for r, m in zip(rs, ms))
-    ss_tot = sum((m - mm) ** 2 for m in ms)
+        print(f"[bench] sweep R={rs[-1]} fwd {ms[-1]:.2f} ms bwd {ms_b[-1]:.2f} ms", file=sys.stderr, flush=True)
     return {
-        "shape": "480p sweep: gen 21x30x52, ref n x 30x52 frames, H=40, d=128, forward",
+        "shape": "480p sweep: gen 21x30x52, ref n x 30x52 frames, H=40, d=128, forward and backward",
         "ref_tokens": rs,
         "ms_fwd": [round(m, 3) for m in ms],
+        "ms_bwd": [round(m, 3) for m in ms_b],
         "visible_pairs_per_head": pairs,
-        "fit_ms_vs_ref_tokens": {"slope_ms_per_1k_tokens": round(slope * 1000, 5), "intercept_ms": round(icpt, 4),
-                                  "r2": round(1 - ss_res / ss_tot, 6) if ss_tot > 0 else 1.0},
+        "fit_ms_vs_ref_tokens": _fit(rs, ms),
+        "fit_bwd_ms_vs_ref_tokens": _fit(rs, ms_b),
         "ms_ratio_last_first": round(ms[-1] / ms[0], 3),
+        "bwd_ms_ratio_last_first": round(ms_b[-1] / ms_b[0], 3),
         "pairs_ratio_last_first": round(pairs[-1] / pairs[0], 3),
     }
 
@@ -218,7 +230,7 @@ def _cpu_baseline(x_gpu, w, gen_rows, torch):
         "cores": threads,
         "kind": "oracle",
         "sample": f"forward (O, LSE) of {rows_g.size} gen + {rows_r.size} ref query rows of head 0 "
-                  f"({n_pairs} visible pairs, {dt:.1f} s, float64 numpy); the oracle has no row-sampled dK/dV",
+                  f"({n_pairs} visible pairs, {dt:.1f} s, float64 numpy); forward only",
     }
 
 
