@@ -244,6 +244,30 @@ def _token_stride(ts, name):
     return 0 if s0 is None else int(s0)
 
 
+def cu_seqlens(samples) -> Tuple[np.ndarray, np.ndarray]:
+    """Packed-row offsets of the samples in each stream: [0, n_0, n_0 + n_1, ...] (int64), as
+    the geometry fixes them (tokens of a sample are packed back to back in sample order)."""
+    g = [0]
+    r = [0]
+    for s in samples:
+        g.append(g[-1] + s.gen_frames * s.gen_h * s.gen_w)
+        r.append(r[-1] + s.ref_frames * s.ref_h * s.ref_w)
+    return np.array(g, dtype=np.int64), np.array(r, dtype=np.int64)
+
+
+def _check_cu_seqlens(samples, cu_gen, cu_ref):
+    """Optional caller-supplied offsets (any sequence or tensor) must equal the geometry's."""
+    if cu_gen is None and cu_ref is None:
+        return
+    want = cu_seqlens(samples)
+    for name, got, w in (("cu_seqlens_gen", cu_gen, want[0]), ("cu_seqlens_ref", cu_ref, want[1])):
+        if got is None:
+            continue
+        a = np.asarray(got.detach().cpu() if hasattr(got, "detach") else got).astype(np.int64).ravel()
+        if not np.array_equal(a, w):
+            raise SRAError(SRA_ERR_INVALID_ARGUMENT, f"{name} {a.tolist()} does not match the geometry {w.tolist()}")
+
+
 def _alloc_workspace(nbytes, device):
     import torch
 
@@ -251,14 +275,17 @@ def _alloc_workspace(nbytes, device):
 
 
 def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[float] = None,
-            out: Optional[Dict] = None, gen_queries_only: bool = False):
+            out: Optional[Dict] = None, gen_queries_only: bool = False, cu_seqlens_gen=None, cu_seqlens_ref=None):
     """SRA forward on the GPU. Returns (o_gen, o_ref, lse_gen, lse_ref).
 
     gen_queries_only: the reference tokens are context only (cached reference K/V); only the
     generation rows are computed, q_ref may be None and o_ref / lse_ref are returned as None.
+    cu_seqlens_gen / cu_seqlens_ref: optional packed-row offsets of the samples; they are
+    checked against the geometry (SRAError with SRA_ERR_INVALID_ARGUMENT on a mismatch).
     """
     import torch
 
+    _check_cu_seqlens(samples, cu_seqlens_gen, cu_seqlens_ref)
     H, d = q_gen.shape[1], q_gen.shape[2]
     dev = q_gen.device
     go = bool(gen_queries_only)
@@ -288,14 +315,17 @@ def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[f
 
 
 def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, lse_ref, do_gen, do_ref,
-             samples, scale: Optional[float] = None, out: Optional[Dict] = None, gen_queries_only: bool = False):
+             samples, scale: Optional[float] = None, out: Optional[Dict] = None, gen_queries_only: bool = False,
+             cu_seqlens_gen=None, cu_seqlens_ref=None):
     """SRA backward on the GPU. Returns dict dq_gen, dk_gen, dv_gen, dq_ref, dk_ref, dv_ref.
 
     gen_queries_only: gradients of the generation rows alone (reference tokens are context
     only); q_ref, o_ref, lse_ref and do_ref may be None and dq_ref is returned as None.
+    cu_seqlens_gen / cu_seqlens_ref: as for forward.
     """
     import torch
 
+    _check_cu_seqlens(samples, cu_seqlens_gen, cu_seqlens_ref)
     H, d = q_gen.shape[1], q_gen.shape[2]
     dev = q_gen.device
     go = bool(gen_queries_only)

@@ -117,3 +117,39 @@ def test_window_flag_constant_and_struct_layout():
     with pytest.raises(sra.SRAError) as e:
         sra.Problem([bad], 1, 64).workspace_size(False)
     assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+
+
+def test_cu_seqlens_are_checked_against_the_geometry():
+    """Optional packed-row offsets must equal the geometry's; a mismatch is rejected before
+    anything reaches the library (CPU tensors here: no device work can happen)."""
+    import numpy as np
+    import torch
+
+    samples = [SampleGeom(1, 2, 4, 2, 2, 2), SampleGeom(2, 2, 2, 0, 1, 1)]
+    g, r = sra.cu_seqlens(samples)
+    assert g.tolist() == [0, 8, 16] and r.tolist() == [0, 8, 8]
+    x = torch.zeros((16, 1, 64), dtype=torch.bfloat16)
+    y = torch.zeros((8, 1, 64), dtype=torch.bfloat16)
+    for bad in ({"cu_seqlens_gen": [0, 8, 17]}, {"cu_seqlens_ref": torch.tensor([0, 4, 8])},
+                {"cu_seqlens_gen": np.array([0, 16])}):
+        with pytest.raises(sra.SRAError) as e:
+            sra.forward(x, x, x, y, y, y, samples, **bad)
+        assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+        with pytest.raises(sra.SRAError):
+            sra.backward(x, x, x, y, y, y, x, y, None, None, x, y, samples, **bad)
+
+
+def test_compacted_plans_reserve_the_compacted_reference_tensors():
+    """A token mask that splits frames runs on the compacted reference stream: the workspace
+    holds 4 (forward) or 8 (backward) compacted [rows, H, d] bf16 tensors more; a mask that
+    only removes whole frames does not."""
+    F, H, d = 16, 2, 64
+    tok = [1, 0] * (F // 2) + [1] * F
+    split = sra.Problem([SampleGeom(1, 4, 4, 2, 4, 4, ref_token_valid=tok)], H, d)
+    plain = sra.Problem([SampleGeom(1, 4, 4, 2, 4, 4)], H, d)
+    whole = sra.Problem([SampleGeom(1, 4, 4, 2, 4, 4, ref_token_valid=[0] * F + [1] * F)], H, d)
+    n_valid = sum(tok)
+    rows = (n_valid * H * d * 2 + 255) // 256 * 256
+    assert split.workspace_size(False) >= plain.workspace_size(False) - 4096 + 4 * rows
+    assert split.workspace_size(True) >= plain.workspace_size(True) - 4096 + 8 * rows
+    assert whole.workspace_size(False) < plain.workspace_size(False) + 4 * rows

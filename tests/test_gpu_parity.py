@@ -354,3 +354,21 @@ def test_gen_queries_only_backward_is_zero_reference_upstream(case):
     want = oracle.sra_backward({k: to_numpy64(v) for k, v in x.items()}, samples)
     for n in ("dq_gen", "dk_gen", "dv_gen", "dk_ref", "dv_ref"):
         assert_close(n, go[n], want[n], 1)
+
+
+def test_matching_cu_seqlens_are_accepted():
+    """Offsets equal to the geometry's (here as device tensors) change nothing."""
+    samples, H, d = CASES["varlen"][0], 2, 128
+    x = make_inputs(samples, H, d, 33)
+    y = {k: v.cuda() for k, v in x.items()}
+    g, r = (torch.as_tensor(c, dtype=torch.int32, device="cuda") for c in sra.cu_seqlens(samples))
+    ins = [y[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
+    a = sra.forward(*ins, samples)
+    b = sra.forward(*ins, samples, cu_seqlens_gen=g, cu_seqlens_ref=r)
+    ga = sra.backward(*ins, *a, y["do_gen"], y["do_ref"], samples)
+    gb = sra.backward(*ins, *a, y["do_gen"], y["do_ref"], samples, cu_seqlens_gen=g, cu_seqlens_ref=r)
+    torch.cuda.synchronize()
+    for t, u in zip(a, b):
+        assert torch.equal(t, u)
+    for n in ga:
+        assert torch.equal(ga[n], gb[n]), n
