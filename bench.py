@@ -224,7 +224,7 @@ def _cpu_baseline(x_gpu, w, gen_rows, torch):
     F = g.ref_h * g.ref_w
     n_pairs = rows_g.size * (G + g.n_ref) + rows_r.size * F * g.group_frames
     flops = 4 * w.head_dim * n_pairs
-    return {
+    out = {
         "value": round(flops / dt / 1e12, 6),
         "unit": "TFLOP/s",
         "cores": threads,
@@ -232,6 +232,28 @@ def _cpu_baseline(x_gpu, w, gen_rows, torch):
         "sample": f"forward (O, LSE) of {rows_g.size} gen + {rows_r.size} ref query rows of head 0 "
                   f"({n_pairs} visible pairs, {dt:.1f} s, float64 numpy); forward only",
     }
+    # the same oracle on one thread against all threads, on the first 128 sampled rows of
+    # each stream
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:  # pragma: no cover
+        return out
+    sub = np.concatenate([rows_g[:128], rows_r[:128]])
+    p1 = rows_g[:128].size * (G + g.n_ref) + rows_r[:128].size * F * g.group_frames
+
+    def run():
+        t = time.perf_counter()
+        oracle.forward_rows(xh, w.samples, 0, 0, sub)
+        return time.perf_counter() - t
+
+    t_all = run()
+    with threadpool_limits(limits=1):
+        t_one = run()
+    out["one_thread"] = {"value": round(4 * w.head_dim * p1 / t_one / 1e12, 6), "unit": "TFLOP/s", "cores": 1,
+                         "all_threads_value": round(4 * w.head_dim * p1 / t_all / 1e12, 6),
+                         "sample": f"forward of the first {rows_g[:128].size} gen + {rows_r[:128].size} ref sampled "
+                                   f"rows of head 0 in one block ({p1} visible pairs, {t_one:.1f} s on one thread)"}
+    return out
 
 
 def _gen_only(sra, torch, ins, fo, w, H, d, reps, line):
