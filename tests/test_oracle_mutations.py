@@ -7,6 +7,7 @@ test_oracle_pins against the mutant and requires it to fail.
 import numpy as np
 import pytest
 
+import oracle
 import oracle.sra_oracle as so
 from sra_inputs import SampleGeom
 
@@ -157,6 +158,55 @@ def bwd_drop_D(q, k, v, do, M, scale):
     return dS @ k * scale, dS.T @ q * scale, P.T @ do, o, lse
 
 
+_orig_dkv = so.dkv_keys
+_orig_dq = so.dq_rows
+
+
+def dkv_unscaled(x, samples, b, h, keys, scale=None, dtype=np.float64, block_rows=4096):
+    # dropped factor: dK without the softmax scale
+    dk, dv = _orig_dkv(x, samples, b, h, keys, scale, dtype, block_rows)
+    d = x["q_gen"].shape[2]
+    return dk / (so.default_scale(d) if scale is None else scale), dv
+
+
+def dkv_swapped(x, samples, b, h, keys, scale=None, dtype=np.float64, block_rows=4096):
+    dk, dv = _orig_dkv(x, samples, b, h, keys, scale, dtype, block_rows)
+    return dv, dk
+
+
+def dkv_last_block_only(x, samples, b, h, keys, scale=None, dtype=np.float64, block_rows=4096):
+    # the block sums overwrite instead of accumulate (only the last query block survives)
+    import torch
+
+    d = x["q_gen"].shape[2]
+    scale = so.default_scale(d) if scale is None else scale
+    cat, _, _ = so._sample_head(x, samples, b, h, dtype)
+    q, do = torch.from_numpy(cat("q_gen", "q_ref")), torch.from_numpy(cat("do_gen", "do_ref"))
+    k, v = torch.from_numpy(cat("k_gen", "k_ref")), torch.from_numpy(cat("v_gen", "v_ref"))
+    kt = torch.from_numpy(np.asarray(keys, dtype=np.int64))
+    dk = torch.zeros((len(keys), d), dtype=q.dtype)
+    dv = torch.zeros((len(keys), d), dtype=q.dtype)
+    for r0 in range(0, q.shape[0], block_rows):
+        rows = np.arange(r0, min(q.shape[0], r0 + block_rows))
+        M = so.visibility_mask(samples[b], rows)
+        sees = M[:, keys].any(axis=1)
+        if not sees.any():
+            continue
+        rows, M = torch.from_numpy(rows[sees]), torch.from_numpy(M[sees])
+        S = ((q[rows] @ k.T) * scale).masked_fill(~M, float("-inf"))
+        P = torch.softmax(S, dim=1)
+        D = (do[rows] * (P @ v)).sum(dim=1, keepdim=True)
+        Pk = P[:, kt]
+        dS = Pk * (do[rows] @ v[kt].T - D)
+        dv = Pk.T @ do[rows]
+        dk = (dS.T @ q[rows]) * scale
+    return dk.numpy(), dv.numpy()
+
+
+def dq_rows_sign(x, samples, b, h, rows, scale=None, dtype=np.float64):
+    return -_orig_dq(x, samples, b, h, rows, scale, dtype)
+
+
 G_INVALID = SampleGeom(3, 2, 4, 5, 2, 5, group_frames=1, frame_valid=[1, 0, 1, 1, 0])
 G_GROUP2 = SampleGeom(1, 4, 4, 6, 3, 3, group_frames=2, frame_valid=[1, 1, 0, 1, 1, 1])
 G_BWD = SampleGeom(2, 2, 2, 3, 2, 2, frame_valid=[1, 0, 1])
@@ -182,6 +232,11 @@ def _all_backward_pins():
     pins.test_backward_matches_torch_autograd_masked_softmax()
 
 
+def _all_sampled_pins():
+    pins.test_row_block_mode_matches_full()
+    pins.test_key_block_mode_matches_full()
+
+
 @pytest.mark.parametrize("attr,mutant,which", [
     ("visibility_mask", mask_gen_drops_ref, "fwd"),
     ("visibility_mask", mask_ref_sees_gen, "fwd"),
@@ -198,13 +253,21 @@ def _all_backward_pins():
     ("attention_backward_full", bwd_sign, "bwd"),
     ("attention_backward_full", bwd_transposed, "bwd"),
     ("attention_backward_full", bwd_drop_D, "bwd"),
+    ("dkv_keys", dkv_unscaled, "sampled"),
+    ("dkv_keys", dkv_swapped, "sampled"),
+    ("dkv_keys", dkv_last_block_only, "sampled"),
+    ("dq_rows", dq_rows_sign, "sampled"),
 ])
 def test_planted_mistake_is_caught(monkeypatch, attr, mutant, which):
     monkeypatch.setattr(so, attr, mutant)
+    if hasattr(oracle, attr):  # names the package re-exports are called through it
+        monkeypatch.setattr(oracle, attr, mutant)
+    run = {"fwd": _all_forward_pins, "bwd": _all_backward_pins, "sampled": _all_sampled_pins}[which]
     with pytest.raises(AssertionError):
-        (_all_forward_pins if which == "fwd" else _all_backward_pins)()
+        run()
 
 
 def test_unmutated_oracle_passes_the_same_pins():
     _all_forward_pins()
     _all_backward_pins()
+    _all_sampled_pins()
