@@ -184,7 +184,7 @@ def _ref_token_ok(geom):
     return ok
 
 
-@pytest.mark.parametrize("name", ["720p", "varlen", "varlen_window", "varlen_tokens"])
+@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "varlen", "varlen_window", "varlen_tokens"])
 def test_fullsize_zero_keys_count_law(name):
     """K = 0 makes every visible logit 0, so LSE = ln(number of visible keys) for every row
     (and -inf for rows of invalid reference tokens)."""
@@ -217,7 +217,7 @@ def test_fullsize_zero_keys_count_law(name):
 IDENTITY_REL = 0.04
 
 
-@pytest.mark.parametrize("name", ["720p", "varlen"])
+@pytest.mark.parametrize("name", ["720p", "varlen", "sweep_256", "varlen_tokens"])
 def test_fullsize_gradient_identities(name):
     """Per sample, head and dim: sum_k dK_k = 0 (each query's dS row sums to 0) and
     sum_k dV_k = sum_q dO_q over valid queries (each query's P row sums to 1), to within
@@ -235,7 +235,9 @@ def test_fullsize_gradient_identities(name):
         def cat(a, c):
             return torch.cat([g[a][go[b]:go[b + 1]], g[c][ro[b]:ro[b + 1]]]).double()
         dk, dv = cat("dk_gen", "dk_ref"), cat("dv_gen", "dv_ref")
-        do = torch.cat([x["do_gen"][go[b]:go[b + 1]], x["do_ref"][ro[b]:ro[b + 1]]]).double()
+        # upstream gradients of the queries that exist (invalid reference tokens are none)
+        ok = torch.as_tensor(_ref_token_ok(w.samples[b]), device=x["do_ref"].device)
+        do = torch.cat([x["do_gen"][go[b]:go[b + 1]], x["do_ref"][ro[b]:ro[b + 1]][ok]]).double()
         rk = dk.sum(0).abs() / dk.pow(2).sum(0).sqrt()              # [H, d]
         rv = (dv.sum(0) - do.sum(0)).abs() / dv.pow(2).sum(0).sqrt()
         print(f"[fullsize] {name} sample {b}: max rel |sum dK| {float(rk.max()):.4f}, "
