@@ -65,8 +65,11 @@ def run_gpu(x, samples, scale=None, backward=True):
     return out
 
 
-def check_against_oracle(samples, H, d, seed, rms=False, scale=None, backward=True):
+def check_against_oracle(samples, H, d, seed, rms=False, scale=None, backward=True, vd_scale=1.0):
     x = make_inputs(samples, H, d, seed, rms_norm_qk=rms)
+    if vd_scale != 1.0:  # a power of two: the scaled bf16 inputs are exact
+        for k in ("v_gen", "v_ref", "do_gen", "do_ref"):
+            x[k] = x[k] * vd_scale
     got = run_gpu(x, samples, scale, backward)
     xo = {k: to_numpy64(v) for k, v in x.items()}
     if backward:
@@ -127,6 +130,18 @@ def test_forward_backward_parity(case):
     samples, H, d, seed, rms = CASES[case]
     print(f"[parity] {case}", flush=True)
     check_against_oracle(samples, H, d, seed, rms)
+
+
+def test_degenerate_sizes():
+    """One gen token, one-token reference frames, a group longer than the clip, a zero-width
+    window over one-token frames, one valid token per frame. With a handful of keys per query
+    the outputs and gradients are O(1) (up to 4 here), where bf16 storage alone is off by up to
+    |x| 2^-9; V and dO are scaled by 1/4 (exact) to keep them in the range the absolute bar
+    was set for."""
+    samples = [SampleGeom(1, 1, 1, 3, 1, 1), SampleGeom(1, 1, 3, 2, 1, 2, group_frames=5),
+               SampleGeom(4, 1, 1, 1, 1, 1, gen_window=0),
+               SampleGeom(1, 2, 2, 3, 2, 3, ref_token_valid=(0, 0, 1, 0, 0, 0) * 3)]
+    check_against_oracle(samples, 3, 64, 34, vd_scale=0.25)
 
 
 def test_custom_scale():
