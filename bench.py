@@ -46,6 +46,7 @@ def _args():
     ap.add_argument("--workload", default="720p", help="720p (default) or varlen")
     ap.add_argument("--sweep-reps", type=int, default=2, help="forward calls per sweep point (0 = skip)")
     ap.add_argument("--cpu-rows", type=int, default=3072, help="gen rows in the CPU-oracle sample (0 = skip)")
+    ap.add_argument("--tiny-reps", type=int, default=200, help="calls per pass of the tiny workload (0 = skip)")
     ap.add_argument("--gen-only-reps", type=int, default=None,
                     help="forward calls timed with the reference as context only (default: --steps; 0 = skip)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -274,6 +275,57 @@ def _gen_only(sra, torch, ins, fo, w, H, d, reps, line):
     print(f"[bench] gen-only forward {go_ms:.2f} ms", file=sys.stderr, flush=True)
 
 
+def _tiny(sra, torch, reps):
+    """The tiny workload (1 head, d = 64, 128 gen + 256 ref tokens): launch- and latency-bound,
+    so it is reported as achieved bytes per second (algorithmic bytes / time), per call (wall
+    time between events, launches included) and per kernel time."""
+    from sra_inputs import make_inputs, workload
+
+    w = workload("tiny")
+    H, d = w.heads, w.head_dim
+    x = make_inputs(w.samples, H, d, w.seed, w.rms_norm_qk, device="cuda", grads=True)
+    ins = [x[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
+    o = sra.forward(*ins, w.samples)
+    fo = {"o_gen": o[0], "o_ref": o[1], "lse_gen": o[2], "lse_ref": o[3]}
+    g = sra.backward(*ins, *o, x["do_gen"], x["do_ref"], w.samples)
+    torch.cuda.synchronize()
+    T = sum(s.n_gen + s.n_ref for s in w.samples)
+    fwd_bytes = T * H * (4 * d * 2 + 4)       # q, k, v read, o written (bf16); lse written
+    bwd_bytes = T * H * (8 * d * 2 + 4)       # q, k, v, o, do read, dq, dk, dv written; lse read
+
+    fo["workspace"] = torch.empty(sra.Problem(w.samples, H, d).workspace_size(False), dtype=torch.uint8,
+                                  device="cuda")
+    g["workspace"] = torch.empty(sra.Problem(w.samples, H, d).workspace_size(True), dtype=torch.uint8,
+                                 device="cuda")
+
+    def run(fn):
+        # wall time per call without the timing events, then the kernels' own time with them
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        sra.kernel_timing_enable(True)
+        for _ in range(reps):
+            fn()
+        kt = sra.kernel_timing()
+        sra.kernel_timing_enable(False)
+        return e0.elapsed_time(e1) / reps, sum(v[0] for v in kt.values()) / reps
+
+    f_call, f_kern = run(lambda: sra.forward(*ins, w.samples, out=fo))
+    b_call, b_kern = run(lambda: sra.backward(*ins, *o, x["do_gen"], x["do_ref"], w.samples, out=g))
+    print(f"[bench] tiny fwd {f_call * 1e3:.1f} us/call, bwd {b_call * 1e3:.1f} us/call", file=sys.stderr, flush=True)
+    return {"workload": "tiny: gen 2x8x8, ref 4x8x8, H=1, d=64", "bound": "launch/latency",
+            "fwd_bytes": fwd_bytes, "bwd_bytes": bwd_bytes,
+            "fwd_us_per_call": round(f_call * 1e3, 2), "fwd_us_kernels": round(f_kern * 1e3, 2),
+            "fwd_gbps_call": round(fwd_bytes / (f_call * 1e-3) / 1e9, 3),
+            "fwd_gbps_kernels": round(fwd_bytes / (f_kern * 1e-3) / 1e9, 3),
+            "bwd_us_per_call": round(b_call * 1e3, 2), "bwd_us_kernels": round(b_kern * 1e3, 2),
+            "bwd_gbps_call": round(bwd_bytes / (b_call * 1e-3) / 1e9, 3),
+            "bwd_gbps_kernels": round(bwd_bytes / (b_kern * 1e-3) / 1e9, 3)}
+
+
 def main():
     args = _args()
     if args.pmc_summary:
@@ -374,6 +426,8 @@ def main():
     torch.cuda.empty_cache()
     if args.sweep_reps > 0:
         line["sweep"] = _sweep(sra, torch, args.sweep_reps)
+    if args.tiny_reps > 0:
+        line["tiny"] = _tiny(sra, torch, args.tiny_reps)
     print(json.dumps(line), flush=True)
 
 
