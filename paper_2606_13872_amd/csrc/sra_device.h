@@ -86,18 +86,4 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const floatx16& v, int base) {
   return r;
 }
 
-// LDS tile layout: row-major tiles of `D` bf16 per row, split into 16-byte chunks whose
-// index is XOR-swizzled by the row. The same tile may be read two ways:
-//  - row fragments (ds_read_b128): 8 consecutive rows, one logical chunk -> the swizzle
-//    maps them to 8 distinct bank groups;
-//  - transpose reads: 4 consecutive rows (4-aligned), 2 adjacent chunks -> 8 distinct
-//    bank groups as well.
-__device__ __forceinline__ int swz(int row) { return ((row & 3) << 1) | ((row >> 2) & 1); }
-
-// Element offset of (row, col) in a swizzled tile of D columns; col % 4 == 0.
-template <int D>
-__device__ __forceinline__ int tile_off(int row, int col) {
-  return row * D + (((col >> 3) ^ swz(row)) << 3) + (col & 7);
-}
-
 }  // namespace sra

@@ -1,45 +1,9 @@
-// Cooperative global -> register -> LDS staging of [rows x D] bf16 tiles (256 threads).
+// Direct global -> LDS staging of padded [rows x D] bf16 tiles and the span walk of the kernels.
 #pragma once
 #include "sra_config.h"
 #include "sra_device.h"
 
 namespace sra {
-
-template <int D, int NR>
-struct TileRegs {
-  static constexpr int kChunksPerRow = D / 8;  // 16-byte chunks
-  static constexpr int kPerThread = NR * kChunksPerRow / kThreads;
-  static_assert(kPerThread * kThreads == NR * kChunksPerRow, "tile must split evenly");
-  uint4 v[kPerThread];
-};
-
-// Loads rows [off, off + NR) of the span [start, start + len) of one head. Rows past the end
-// of the span are clamped to its last row, so every address stays inside the tensor; the
-// kernels mask those rows out of the softmax.
-template <int D, int NR>
-__device__ __forceinline__ void tile_load(TileRegs<D, NR>& t, const __bf16* __restrict__ src,
-                                          int64_t stride, int head, int start, int len, int off) {
-  constexpr int CPR = TileRegs<D, NR>::kChunksPerRow;
-#pragma unroll
-  for (int i = 0; i < TileRegs<D, NR>::kPerThread; ++i) {
-    const int u = int(threadIdx.x) + i * kThreads;
-    const int r = u / CPR, ch = u % CPR;
-    const int rr = min(off + r, len - 1);
-    const __bf16* g = src + int64_t(start + rr) * stride + head * D + ch * 8;
-    t.v[i] = *reinterpret_cast<const uint4*>(g);
-  }
-}
-
-template <int D, int NR>
-__device__ __forceinline__ void tile_store(const TileRegs<D, NR>& t, __bf16* lds) {
-  constexpr int CPR = TileRegs<D, NR>::kChunksPerRow;
-#pragma unroll
-  for (int i = 0; i < TileRegs<D, NR>::kPerThread; ++i) {
-    const int u = int(threadIdx.x) + i * kThreads;
-    const int r = u / CPR, ch = u % CPR;
-    *reinterpret_cast<uint4*>(lds + tile_off<D>(r, ch * 8)) = t.v[i];
-  }
-}
 
 // Padded LDS tiles: NR rows of D bf16 with a row stride of RS elements, so every fragment
 // address is one per-lane base plus a compile-time offset. The stride decides the bank
@@ -96,22 +60,6 @@ __device__ __forceinline__ uint64_t uniform_u64(uint64_t x) {
   const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(x));
   const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(x >> 32));
   return (uint64_t(hi) << 32) | lo;
-}
-
-// One dword per lane: lane l's 4 bytes land at (LDS base + 4 l).
-__device__ __forceinline__ void lds_dma_x1(const void* g, void* lds) {
-  const uint32_t la = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds);
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dword %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(g), "s"(la)
-      : "memory");
 }
 
 // LDS byte address of a __shared__ object.
