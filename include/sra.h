@@ -155,7 +155,9 @@ sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, ui
 
 /* Copies schedule `which` into host buffers: items[8*i + 0..7] = {stream, head, start, length,
  * span_offset, span_count, sample, reserved} per work item, spans[4*j + 0..3] = {stream,
- * start, length, reserved} per span (stream 0 = gen, 1 = ref; start = packed token row).
+ * start, length, keys} per span (stream 0 = gen, 1 = ref; start = packed token row; keys, in
+ * the dK/dV schedule only: the item's keys [lo, hi), counted from its first key, that the
+ * span's queries see, packed lo | hi << 16, or 0 for all of them).
  * items/spans may be NULL to query only; capacities count int32 elements.
  * When token masks split reference frames into more runs of valid tokens than there are
  * groups with a valid token, the library runs on the compacted reference stream (the valid

@@ -6,11 +6,13 @@
 // carries a token mask, its own entry is (§4.3 invalid tokens). The rule is expressed here
 // as contiguous row ranges ("spans") built from the runs of valid ref rows, so each work
 // item's kernel loop visits only visible key (or query) rows and masks nothing but the
-// ragged end of a span.
+// ragged end of a span and, in the key-major schedule, the keys of a tile that a group's
+// reference queries do not reach.
 #include "schedule.hpp"
 
 #include <algorithm>
 #include <cmath>
+#include <map>
 #include <cstdio>
 #include <numeric>
 
@@ -263,10 +265,31 @@ void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
   order_items(v, L.heads, s);
 }
 
+// First frame of the ref group holding sample-relative ref row r.
+int32_t group_of_row(const SampleLayout& s, int64_t r) {
+  if (!s.gbound.empty()) {
+    const auto it = std::upper_bound(s.gbound.begin(), s.gbound.end(), r);
+    return int32_t(it - s.gbound.begin() - 1) * s.group;
+  }
+  return int32_t(r / s.F) / s.group * s.group;
+}
+
 // Key-major schedule (dK/dV): key tiles, query spans per class.
 void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
   std::vector<TileClass> classes;
+  std::vector<std::pair<int64_t, WorkItem>> v;
   s->spans.clear();
+  std::map<std::vector<int32_t>, int32_t> lists;  // span list (flattened) -> offset
+  auto intern = [&](const std::vector<Span>& l) {
+    std::vector<int32_t> key;
+    for (const Span& x : l) key.insert(key.end(), {x.stream, x.start, x.len, x.keys});
+    auto it = lists.find(key);
+    if (it != lists.end()) return it->second;
+    const int32_t off = int32_t(s->spans.size());
+    s->spans.insert(s->spans.end(), l.begin(), l.end());
+    lists.emplace(std::move(key), off);
+    return off;
+  };
   for (int32_t b = 0; b < L.batch; ++b) {
     const SampleLayout& sm = L.samples[b];
     // gen keys are seen by the gen queries of the sample only (those of the frames within the
@@ -284,22 +307,43 @@ void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
         classes.push_back({0, sm.gen_off + t * sm.Fg, sm.Fg, gq, 1, b, 0});
       }
     }
-    // valid ref keys: gen queries + the valid ref queries of their group
-    for (int32_t g0 = 0; g0 < sm.ref_frames; g0 += sm.group) {
-      const RowRun gr = group_rows(sm, g0);
-      std::vector<RowRun> runs = valid_runs(sm, gr.r0, gr.r1);
-      if (runs.empty()) continue;
-      int32_t off = int32_t(s->spans.size());
-      s->spans.push_back({0, int32_t(sm.gen_off), int32_t(sm.G), 0});
-      if (!L.gen_only)
-        for (const RowRun& r : runs)
-          s->spans.push_back({1, int32_t(sm.ref_off + r.r0), int32_t(r.r1 - r.r0), 0});
-      const int32_t cnt = int32_t(s->spans.size()) - off;
-      for (const RowRun& r : runs)
-        classes.push_back({1, sm.ref_off + r.r0, r.r1 - r.r0, off, cnt, b, 0});
+    // valid ref keys are seen by every gen query of the sample and by the valid ref queries of
+    // their group. Tiles run across group boundaries inside each run of valid rows (a group's
+    // last tile would otherwise be mostly empty and still stream every gen query); a tile's
+    // span for one group's ref queries carries the range of the tile's keys in that group.
+    for (const auto& run : sm.vruns) {
+      for (int64_t a = run.first; a < run.second; a += tile) {
+        const int64_t e = std::min<int64_t>(a + tile, run.second);
+        std::vector<Span> l{{0, int32_t(sm.gen_off), int32_t(sm.G), 0}};
+        if (!L.gen_only) {
+          for (int32_t g0 = group_of_row(sm, a); g0 < sm.ref_frames; g0 += sm.group) {
+            const RowRun gr = group_rows(sm, g0);
+            if (gr.r0 >= e) break;
+            const int64_t lo = std::max(a, gr.r0), hi = std::min(e, gr.r1);
+            if (lo >= hi) continue;
+            const int32_t keys = (lo == a && hi == e) ? 0 : int32_t(((hi - a) << 16) | (lo - a));
+            for (const RowRun& q : valid_runs(sm, gr.r0, gr.r1))
+              l.push_back({1, int32_t(sm.ref_off + q.r0), int32_t(q.r1 - q.r0), keys});
+          }
+        }
+        const int32_t off = intern(l);
+        int64_t step_rows = 0;
+        for (const Span& x : l) step_rows += (x.len + step - 1) / step * step;
+        for (int32_t h = 0; h < L.heads; ++h) {
+          WorkItem w;
+          w.stream = 1;
+          w.head = h;
+          w.start = int32_t(sm.ref_off + a);
+          w.len = int32_t(e - a);
+          w.span_off = off;
+          w.span_cnt = int32_t(l.size());
+          w.sample = b;
+          w.reserved = 0;
+          v.push_back({int64_t(tile) * step_rows, w});
+        }
+      }
     }
   }
-  std::vector<std::pair<int64_t, WorkItem>> v;
   for (const TileClass& c : classes) emit_items(c, tile, L.heads, step, s->spans, &v);
   order_items(v, L.heads, s);
 }
@@ -373,9 +417,11 @@ int64_t covered_pairs(const Schedule& s, bool /*key_major*/) {
   int64_t n = 0;
   for (const WorkItem& w : s.items) {
     if (w.stream < 0 || w.head != 0) continue;
-    int64_t other = 0;
-    for (int32_t i = 0; i < w.span_cnt; ++i) other += s.spans[w.span_off + i].len;
-    n += int64_t(w.len) * other;
+    for (int32_t i = 0; i < w.span_cnt; ++i) {
+      const Span& x = s.spans[w.span_off + i];
+      const int64_t keys = x.keys ? (x.keys >> 16) - (x.keys & 0xffff) : w.len;
+      n += keys * x.len;
+    }
   }
   return n;
 }

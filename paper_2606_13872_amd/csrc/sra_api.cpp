@@ -603,7 +603,10 @@ sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, ui
     if (w.stream < 0 || w.head != 0 || w.sample != sample) continue;
     for (int32_t si = 0; si < w.span_cnt; ++si) {
       const Span& sp = S->spans[w.span_off + si];
-      for (int32_t a = 0; a < w.len; ++a) {
+      // a key-major span may reach only the item's keys [lo, hi)
+      const int32_t a0 = sp.keys ? (sp.keys & 0xffff) : 0, a1 = sp.keys ? (sp.keys >> 16) : w.len;
+      if (a0 < 0 || a1 > w.len || a0 >= a1) return fail(SRA_ERR_INTERNAL, "span key range outside its item");
+      for (int32_t a = a0; a < a1; ++a) {
         const int64_t ta = local(w.stream, int64_t(w.start) + a);
         for (int32_t b = 0; b < sp.len; ++b) {
           const int64_t tb = local(sp.stream, int64_t(sp.start) + b);

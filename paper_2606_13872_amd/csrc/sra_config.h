@@ -36,7 +36,8 @@ struct Span {
   int32_t stream;      // 0 = generation, 1 = reference
   int32_t start;       // first packed token row
   int32_t len;         // rows (> 0)
-  int32_t reserved;
+  int32_t keys;        // key-major schedules: the work item's keys [lo, hi) (tile-relative) this
+                       // span reaches, packed lo | hi << 16; 0 = every key of the item
 };
 
 // Row range of a stream whose outputs are constant (invalid reference frames).

@@ -33,11 +33,12 @@ struct DkvState {
 // run in four phases of NC slots (S, dP, dV, dK); each slot issues the LDS reads of the next
 // slot, two MFMAs and a share of the VALU work (the exponentials during dP, dS during dV),
 // and ends at a scheduling barrier so the compiler keeps that interleave and the register
-// footprint of one slot. kMask: query rows >= nvalid are outside the span.
+// footprint of one slot. kMask: query rows >= nvalid are outside the span, and the lane's key of
+// block j takes part only if kvj (a span that reaches only part of the tile's keys).
 template <int D, bool kMask>
 __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, const __bf16* qt,
                                          const __bf16* dt, const float* lse_s, const float* ndlt_s,
-                                         int nvalid, float sl2) {
+                                         int nvalid, float sl2, bool kv0 = true, bool kv1 = true) {
   constexpr int NC = D / 16, ND = D / 32, RQ = kRowPadRS<D>, RK = kRowPadRS<D>;  // Q, dO rows permuted
   constexpr int EP = 32 / NC;  // P (or dS) elements per slot, over both blocks
   const int lane = threadIdx.x & 63, half = lane >> 5, l32 = lane & 31;
@@ -99,11 +100,11 @@ __device__ __forceinline__ void dkv_step(DkvState<D>& st, const __bf16* krow, co
       const int x = c * EP + u, i = x % 16, q = 8 * (i / 4) + 4 * half + (i % 4);
       if (x < 16) {
         float p = fast_exp2(fmaf(s0[i], sl2, -l4[i / 4][i % 4]));
-        if constexpr (kMask) p = q < nvalid ? p : 0.f;
+        if constexpr (kMask) p = (q < nvalid && kv0) ? p : 0.f;
         s0[i] = p;
       } else {
         float p = fast_exp2(fmaf(s1[i], sl2, -l4[i / 4][i % 4]));
-        if constexpr (kMask) p = q < nvalid ? p : 0.f;
+        if constexpr (kMask) p = (q < nvalid && kv1) ? p : 0.f;
         s1[i] = p;
       }
     }
@@ -274,7 +275,13 @@ sra_dkv_kernel(BwdArgs a) {
   int t = 0;
   for (int si = 0; si < it.span_cnt; ++si) {
     const int len = __builtin_amdgcn_readfirstlane(sp[si].len);
-    const int full = len / BQ;
+    // a span may reach only the tile's keys [lo, hi) (the reference queries of one group, on a
+    // tile that crosses into the next group): then every step of it is masked
+    const int kr = __builtin_amdgcn_readfirstlane(sp[si].keys);
+    const int klo = kr & 0xffff, khi = kr ? (kr >> 16) : kDkvKeyTile;
+    const int key0 = wave * 64 + l32;
+    const bool kv0 = key0 >= klo && key0 < khi, kv1 = key0 + 32 >= klo && key0 + 32 < khi;
+    const int full = kr ? 0 : len / BQ;
     for (int j = 0; j < full; ++j, ++t) {
       const int b = t % NB;
       if (t + 2 < T) issue((t + 2) % NB, t + 2);
@@ -282,13 +289,13 @@ sra_dkv_kernel(BwdArgs a) {
       if (t + 2 < T) put_stat(t + 2);
       step_tail(t);
     }
-    if (len % BQ) {
+    for (int off = full * BQ; off < len; off += BQ, ++t) {
       const int b = t % NB;
       if (t + 2 < T) issue((t + 2) % NB, t + 2);
-      if (active) dkv_step<D, true>(st, krow, qs[b], dos[b], rstat[b], rstat[b] + BQ, len % BQ, sl2);
+      if (active)
+        dkv_step<D, true>(st, krow, qs[b], dos[b], rstat[b], rstat[b] + BQ, min(BQ, len - off), sl2, kv0, kv1);
       if (t + 2 < T) put_stat(t + 2);
       step_tail(t);
-      ++t;
     }
   }
 
