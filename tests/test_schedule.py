@@ -177,3 +177,27 @@ def test_token_masks_that_split_frames_run_on_the_compacted_stream():
     it = items[items[:, 0] == 0][0]
     own = spans[it[4]:it[4] + it[5]]
     assert [tuple(r[1:3]) for r in own[own[:, 0] == 1]] == [(0, F), (2 * F, F)]
+
+
+def test_key_tiles_cross_reference_groups_with_key_ranges():
+    """dK/dV tiles of reference keys run across frames (groups) inside a run of valid rows; each
+    group's reference-query span of a crossing tile carries the range of the tile's keys in
+    that group, so every (query, key) pair is still covered exactly once."""
+    F = 100  # 10 x 10 tokens per frame: a 256-key tile spans three frames
+    samples = [SampleGeom(1, 4, 4, 5, 10, 10)]
+    items, spans = sra.schedule_export(samples, sra.SCHED_BWD_DKDV)
+    ref = items[(items[:, 0] == 1) & (items[:, 1] == 0)]
+    assert sorted(ref[:, 2].tolist()) == [0, 256]          # 500 ref keys: tiles of 256 and 244
+    ranged = []
+    for it in ref:
+        for sp in spans[it[4]:it[4] + it[5]]:
+            if sp[0] == 1:
+                lo, hi = sp[3] & 0xFFFF, sp[3] >> 16
+                if sp[3] == 0:
+                    lo, hi = 0, it[3]
+                # the span's queries are the frame holding the tile's keys [lo, hi)
+                f = (it[2] + lo) // F
+                assert sp[1] == f * F and sp[2] == F and (it[2] + hi - 1) // F == f
+                ranged.append((it[2] + lo, it[2] + hi))
+    assert sorted(ranged) == [(0, 100), (100, 200), (200, 256), (256, 300), (300, 400), (400, 500)]
+    assert sra.schedule_info(samples, sra.SCHED_BWD_DKDV)[2] == sum(sra.pair_counts(samples))
