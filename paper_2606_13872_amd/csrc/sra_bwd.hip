@@ -9,7 +9,8 @@
 //           two kernels fetch both per row and use them without further arithmetic.
 //   dq    : query-major, in sra_dq.hip.
 //   dkv   : key-major, in sra_dkv.hip.
-// P is recomputed from the forward's log-sum-exp. Spans' ragged ends are the only masks.
+// P is recomputed from the forward's log-sum-exp. Spans' ragged ends, and in dK/dV the keys of
+// a tile outside a span's key range, are the only masks.
 #include "sra_kernels.h"
 #include "sra_tiles.h"
 

@@ -4,7 +4,8 @@
 // SIMD) own 64 keys each, as two 32-key MFMA blocks, and keep those keys' V in VGPRs and their
 // dK and dV sums in AGPRs for the whole item. K sits in LDS. The query rows that see the keys
 // stream through LDS 32 at a time (gen keys: the gen queries of the sample; ref keys: the gen
-// queries plus the ref queries of the key's group):
+// queries plus the ref queries of the key's group; a tile may hold keys of two groups, and
+// then each group's query span reaches only its own range of the tile's keys):
 //     S = Q K^T, dP = dO V^T, P = exp2(S scale log2e - LSE), dS = P (dP - D),
 //     dV^T += dO^T P, dK^T += Q^T dS.
 // Each Q and dO fragment read from LDS feeds both key blocks of a wave, which halves the LDS
