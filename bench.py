@@ -278,7 +278,9 @@ def _gen_only(sra, torch, ins, fo, w, H, d, reps, line):
 def _tiny(sra, torch, reps):
     """The tiny workload (1 head, d = 64, 128 gen + 256 ref tokens): launch- and latency-bound,
     so it is reported as achieved bytes per second (algorithmic bytes / time), per call (wall
-    time between events, launches included) and per kernel time."""
+    time between events, launches included) and per kernel time; the host's own time per call
+    (Python binding, C entry point and launches, without waiting for the GPU) is given beside
+    them."""
     from sra_inputs import make_inputs, workload
 
     w = workload("tiny")
@@ -302,8 +304,10 @@ def _tiny(sra, torch, reps):
         # wall time per call without the timing events, then the kernels' own time with them
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
+        t = time.perf_counter()
         for _ in range(reps):
             fn()
+        host = (time.perf_counter() - t) * 1e3 / reps
         e1.record()
         torch.cuda.synchronize()
         sra.kernel_timing_enable(True)
@@ -311,16 +315,17 @@ def _tiny(sra, torch, reps):
             fn()
         kt = sra.kernel_timing()
         sra.kernel_timing_enable(False)
-        return e0.elapsed_time(e1) / reps, sum(v[0] for v in kt.values()) / reps
+        return e0.elapsed_time(e1) / reps, sum(v[0] for v in kt.values()) / reps, host
 
-    f_call, f_kern = run(lambda: sra.forward(*ins, w.samples, out=fo))
-    b_call, b_kern = run(lambda: sra.backward(*ins, *o, x["do_gen"], x["do_ref"], w.samples, out=g))
+    f_call, f_kern, f_host = run(lambda: sra.forward(*ins, w.samples, out=fo))
+    b_call, b_kern, b_host = run(lambda: sra.backward(*ins, *o, x["do_gen"], x["do_ref"], w.samples, out=g))
     print(f"[bench] tiny fwd {f_call * 1e3:.1f} us/call, bwd {b_call * 1e3:.1f} us/call", file=sys.stderr, flush=True)
     return {"workload": "tiny: gen 2x8x8, ref 4x8x8, H=1, d=64", "bound": "launch/latency",
             "fwd_bytes": fwd_bytes, "bwd_bytes": bwd_bytes,
             "fwd_us_per_call": round(f_call * 1e3, 2), "fwd_us_kernels": round(f_kern * 1e3, 2),
             "fwd_gbps_call": round(fwd_bytes / (f_call * 1e-3) / 1e9, 3),
             "fwd_gbps_kernels": round(fwd_bytes / (f_kern * 1e-3) / 1e9, 3),
+            "fwd_us_host": round(f_host * 1e3, 2), "bwd_us_host": round(b_host * 1e3, 2),
             "bwd_us_per_call": round(b_call * 1e3, 2), "bwd_us_kernels": round(b_kern * 1e3, 2),
             "bwd_gbps_call": round(bwd_bytes / (b_call * 1e-3) / 1e9, 3),
             "bwd_gbps_kernels": round(bwd_bytes / (b_kern * 1e-3) / 1e9, 3)}

@@ -31,6 +31,10 @@
  *             returns an error has written nothing. sra_last_error() gives a per-thread
  *             message. No C++ exception crosses this boundary. All functions are thread safe.
  *   Supported head_dim in {64, 128}; heads >= 1; batch >= 1; every sample has >= 1 gen token.
+ *   Limits    packed tokens of each stream <= 2^31 - 1 (beyond: SRA_ERR_INVALID_ARGUMENT);
+ *             num_heads * packed tokens of each stream <= 2^31 - 1 (beyond: SRA_ERR_UNSUPPORTED;
+ *             per-row statistics are indexed in 32 bits). Tensors themselves may exceed 2^31
+ *             elements: token offsets are 64-bit.
  */
 #ifndef SRA_H_
 #define SRA_H_

@@ -137,6 +137,12 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
       return SRA_ERR_INVALID_ARGUMENT;
     }
   }
+  // The kernels index per-row statistics (log-sum-exp, -rowsum(dO * O)) as head * rows + row
+  // and whole token rows as heads * head_dim elements, both in 32 bits.
+  if (hd > kRowLimit || int64_t(L.heads) * std::max(L.sum_gen, L.sum_ref) > kRowLimit) {
+    *err = "num_heads * packed tokens of a stream (or num_heads * head_dim) exceeds 2^31 - 1";
+    return SRA_ERR_UNSUPPORTED;
+  }
   *out = std::move(L);
   return SRA_OK;
 }

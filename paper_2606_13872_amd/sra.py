@@ -268,6 +268,14 @@ def _check_cu_seqlens(samples, cu_gen, cu_ref):
             raise SRAError(SRA_ERR_INVALID_ARGUMENT, f"{name} {a.tolist()} does not match the geometry {w.tolist()}")
 
 
+def _out(out, name, shape, dtype, device):
+    """The caller's output buffer `name`, or a new one (allocated only when none was given)."""
+    import torch
+
+    t = out.get(name)
+    return torch.empty(shape, dtype=dtype, device=device) if t is None else t
+
+
 def _alloc_workspace(nbytes, device):
     import torch
 
@@ -297,13 +305,13 @@ def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[f
     if q_gen.shape[0] != p.n_gen or (k_ref is not None and k_ref.shape[0] != p.n_ref):
         raise ValueError("token counts do not match the geometry")
     out = out or {}
-    o_gen = out.get("o_gen", torch.empty((p.n_gen, H, d), dtype=torch.bfloat16, device=dev))
-    lse_gen = out.get("lse_gen", torch.empty((H, p.n_gen), dtype=torch.float32, device=dev))
+    o_gen = _out(out, "o_gen", (p.n_gen, H, d), torch.bfloat16, dev)
+    lse_gen = _out(out, "lse_gen", (H, p.n_gen), torch.float32, dev)
     if go:
         q_ref = o_ref = lse_ref = None
     else:
-        o_ref = out.get("o_ref", torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
-        lse_ref = out.get("lse_ref", torch.empty((H, p.n_ref), dtype=torch.float32, device=dev))
+        o_ref = _out(out, "o_ref", (p.n_ref, H, d), torch.bfloat16, dev)
+        lse_ref = _out(out, "lse_ref", (H, p.n_ref), torch.float32, dev)
     nbytes = p.workspace_size(False)
     ws = out.get("workspace")
     if ws is None or ws.numel() < nbytes:
@@ -339,10 +347,10 @@ def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, ls
     out = out or {}
     g = {}
     for n in ("dq_gen", "dk_gen", "dv_gen"):
-        g[n] = out.get(n, torch.empty((p.n_gen, H, d), dtype=torch.bfloat16, device=dev))
+        g[n] = _out(out, n, (p.n_gen, H, d), torch.bfloat16, dev)
     for n in ("dq_ref", "dk_ref", "dv_ref"):
         g[n] = None if (go and n == "dq_ref") else \
-            out.get(n, torch.empty((p.n_ref, H, d), dtype=torch.bfloat16, device=dev))
+            _out(out, n, (p.n_ref, H, d), torch.bfloat16, dev)
     nbytes = p.workspace_size(True)
     ws = out.get("workspace")
     if ws is None or ws.numel() < nbytes:

@@ -39,10 +39,23 @@ GOOD = [SampleGeom(2, 8, 8, 4, 8, 8)]
     (GOOD, 2, 64, 64, sra.SRA_ERR_INVALID_ARGUMENT),      # stride < H*d
     (GOOD, 2, 64, 132, sra.SRA_ERR_INVALID_ARGUMENT),     # stride not a multiple of 8
     ([SampleGeom(70000, 200, 200, 0, 1, 1)], 1, 64, 0, sra.SRA_ERR_INVALID_ARGUMENT),  # > int32 rows
+    # heads * rows above 2^31 - 1: 40 heads x 53,687,092 gen rows, then 40 x that many ref rows
+    ([SampleGeom(1, 53687092, 1, 0, 1, 1)], 40, 128, 0, sra.SRA_ERR_UNSUPPORTED),
+    ([SampleGeom(1, 1, 1, 1, 53687092, 1)], 40, 128, 0, sra.SRA_ERR_UNSUPPORTED),
+    # the largest accepted: heads * rows = 2^31 - 1 exactly (gen), and just below (ref)
+    ([SampleGeom(1, 2147483647, 1, 0, 1, 1)], 1, 64, 0, None),
+    ([SampleGeom(1, 1, 1, 1, 53687091, 1)], 40, 128, 0, None),
 ])
 def test_invalid_problems_are_rejected(samples, heads, d, stride, status):
     p = sra.Problem(samples, heads, d, gen_token_stride=stride)
     n = ctypes.c_size_t(0)
+    if status is None:  # at the limit: accepted (checked on the geometry only, no schedule)
+        gp, rp = ctypes.c_int64(0), ctypes.c_int64(0)
+        assert sra.lib().sra_pair_counts(p.ptr, ctypes.byref(gp), ctypes.byref(rp)) == sra.SRA_OK
+        G, R = p.n_gen, p.n_ref
+        F = samples[0].ref_h * samples[0].ref_w
+        assert (gp.value, rp.value) == (G * (G + R), R * F)
+        return
     st = sra.lib().sra_workspace_size(p.ptr, 0, ctypes.byref(n))
     assert st == status
     assert len(sra.lib().sra_last_error()) > 0
