@@ -9,8 +9,10 @@ HBM: 1 sample, generation 21x45x80 = 75,600 tokens, reference 21x45x80 = 75,600 
 Prints ONE JSON line. value = useful TFLOP/s of the step: only visible query-key pairs
 count, 4*d FLOP per pair forward and 10*d backward. Also reported: % of the bf16 dense
 MFMA peak, ms per layer forward/backward, the roofline of the dominant kernel (timed with
-hipEvents on its launch stream inside the library), the forward time against reference
-length at the 480p sweep shape, and the CPU oracle on a bounded sample.
+hipEvents on its launch stream inside the library), forward and backward time against
+reference length at the 480p sweep shape, the 480p layer and the varlen packed batch (also
+with the temporal window and with reference token masks) per call, the tiny workload as
+achieved bytes per second, and the CPU oracle on a bounded sample.
 """
 from __future__ import annotations
 
@@ -47,6 +49,8 @@ def _args():
     ap.add_argument("--sweep-reps", type=int, default=2, help="forward calls per sweep point (0 = skip)")
     ap.add_argument("--cpu-rows", type=int, default=3072, help="gen rows in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--tiny-reps", type=int, default=200, help="calls per pass of the tiny workload (0 = skip)")
+    ap.add_argument("--other-reps", type=int, default=2,
+                    help="timed calls per pass of the 480p and varlen workloads (0 = skip)")
     ap.add_argument("--gen-only-reps", type=int, default=None,
                     help="forward calls timed with the reference as context only (default: --steps; 0 = skip)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -195,6 +199,49 @@ def _sweep(sra, torch, reps):
         "bwd_ms_ratio_last_first": round(ms_b[-1] / ms_b[0], 3),
         "pairs_ratio_last_first": round(pairs[-1] / pairs[0], 3),
     }
+
+
+def _other_workloads(sra, torch, reps):
+    """The other full-size workloads, one forward and one backward call each: the 480p layer,
+    the varlen packed batch, and that batch with the refiner's temporal window and with
+    reference token masks. ms per call and useful TFLOP/s (visible pairs only)."""
+    from sra_inputs import make_inputs, workload
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    res = {}
+    for name in ("480p", "varlen", "varlen_window", "varlen_tokens"):
+        w = workload(name)
+        H, d = w.heads, w.head_dim
+        x = make_inputs(w.samples, H, d, w.seed, w.rms_norm_qk, device="cuda", grads=True)
+        args = [x[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
+        o = sra.forward(*args, w.samples)
+        out = {"o_gen": o[0], "o_ref": o[1], "lse_gen": o[2], "lse_ref": o[3]}
+        g = sra.backward(*args, *o, x["do_gen"], x["do_ref"], w.samples)
+        ms_f = timed(lambda: sra.forward(*args, w.samples, out=out))
+        ms_b = timed(lambda: sra.backward(*args, *o, x["do_gen"], x["do_ref"], w.samples, out=g))
+        ff, bf = sra.useful_flops(w.samples, H, d)
+        cfg = _workload_config(w)
+        res[name] = {"workload": cfg["workload"].replace(", group=1 frame, forward+backward", ""),
+                     "gen_tokens": cfg["gen_tokens"], "ref_tokens": cfg["ref_tokens"],
+                     "visible_pairs": ff // (4 * d),
+                     "ms_fwd": round(ms_f, 3), "ms_bwd": round(ms_b, 3),
+                     "fwd_tflops": round(ff / (ms_f * 1e-3) / 1e12, 2),
+                     "bwd_tflops": round(bf / (ms_b * 1e-3) / 1e12, 2),
+                     "pct_bf16_peak": round(100 * (ff + bf) / ((ms_f + ms_b) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 2)}
+        del x, out, args, o, g
+        torch.cuda.empty_cache()
+        print(f"[bench] {name} fwd {ms_f:.2f} ms bwd {ms_b:.2f} ms", file=sys.stderr, flush=True)
+    return res
 
 
 def _cpu_baseline(x_gpu, w, gen_rows, torch):
@@ -431,6 +478,8 @@ def main():
     torch.cuda.empty_cache()
     if args.sweep_reps > 0:
         line["sweep"] = _sweep(sra, torch, args.sweep_reps)
+    if args.other_reps > 0:
+        line["other_workloads"] = _other_workloads(sra, torch, args.other_reps)
     if args.tiny_reps > 0:
         line["tiny"] = _tiny(sra, torch, args.tiny_reps)
     print(json.dumps(line), flush=True)
