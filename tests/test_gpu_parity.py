@@ -387,3 +387,28 @@ def test_matching_cu_seqlens_are_accepted():
         assert torch.equal(t, u)
     for n in ga:
         assert torch.equal(ga[n], gb[n]), n
+
+
+def test_caller_buffers_are_filled_in_place():
+    """Outputs the caller passes (some of them, plus a workspace) are written in place and
+    returned; the missing ones are allocated. Results equal those of a call without buffers."""
+    samples, H, d = CASES["varlen"][0], 2, 128
+    x = make_inputs(samples, H, d, 34)
+    y = {k: v.cuda() for k, v in x.items()}
+    ins = [y[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
+    a = sra.forward(*ins, samples)
+    ga = sra.backward(*ins, *a, y["do_gen"], y["do_ref"], samples)
+    p = sra.Problem(samples, H, d)
+    fo = {"o_gen": torch.full_like(a[0], float("nan")), "lse_ref": torch.full_like(a[3], float("nan")),
+          "workspace": torch.empty(p.workspace_size(False), dtype=torch.uint8, device="cuda")}
+    b = sra.forward(*ins, samples, out=fo)
+    assert b[0] is fo["o_gen"] and b[3] is fo["lse_ref"]
+    bo = {"dq_gen": torch.full_like(ga["dq_gen"], float("nan")), "dv_ref": torch.full_like(ga["dv_ref"], float("nan")),
+          "workspace": torch.empty(p.workspace_size(True), dtype=torch.uint8, device="cuda")}
+    gb = sra.backward(*ins, *a, y["do_gen"], y["do_ref"], samples, out=bo)
+    assert gb["dq_gen"] is bo["dq_gen"] and gb["dv_ref"] is bo["dv_ref"]
+    torch.cuda.synchronize()
+    for t, u in zip(a, b):
+        assert torch.equal(t, u)
+    for n in ga:
+        assert torch.equal(ga[n], gb[n]), n
