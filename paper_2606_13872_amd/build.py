@@ -27,7 +27,7 @@ COMMON = [
 ]
 # Device code only for gfx950. Packed-FP32 instructions are disabled in device code.
 HIP_FLAGS = ["-x", "hip", "--offload-arch=gfx950", "-Xclang", "-target-feature",
-             "-Xclang", "-packed-fp32-ops", "-munsafe-fp-atomics"]
+             "-Xclang", "-packed-fp32-ops"]
 # The dK/dV and dQ kernels select their compiler-visible MFMAs in VGPR form: their AGPRs hold
 # the gradient sums (written by inline-assembly MFMAs), and S/dP must stay in VGPRs next to them.
 _VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]

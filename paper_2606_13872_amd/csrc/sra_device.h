@@ -63,17 +63,6 @@ __device__ __forceinline__ bf16x8 cat8(bf16x4 lo, bf16x4 hi) {
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// Sum of the 8 bf16 values of a fragment added to acc (fp32), two per V_DOT2C_F32_BF16.
-__device__ __forceinline__ float sum_bf16x8(bf16x8 v, float acc) {
-  const bf16x2 one = {(__bf16)1.0f, (__bf16)1.0f};
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const bf16x2 p = {v[2 * j], v[2 * j + 1]};
-    acc = __builtin_amdgcn_fdot2_f32_bf16(p, one, acc, false);
-  }
-  return acc;
-}
-
 // IEEE-2019 maximum (V_MAXIMUM3_F32 on gfx950): needs no NaN canonicalisation of MFMA results.
 __device__ __forceinline__ float max2f(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 __device__ __forceinline__ float max3f(float a, float b, float c) { return max2f(a, max2f(b, c)); }
