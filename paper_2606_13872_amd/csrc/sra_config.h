@@ -8,15 +8,16 @@ namespace sra {
 // item covers 256 query rows; keys stream through LDS 64 at a time.
 constexpr int kFwdQueryTile = 256;
 constexpr int kFwdKeyStep = 64;
-// dQ kernel of the backward: same query tiling (8 waves x 32 rows), 32-key steps.
+// dQ kernel of the backward: 256-row query tiles as in the forward, held by 4 wave64s (one per
+// SIMD, 64 query rows each); keys stream through LDS 32 at a time.
 constexpr int kDqQueryTile = 256;
 constexpr int kDqKeyStep = 32;
-// dK/dV kernel of the backward: 8 waves x 32 keys = 256 keys per work item; queries stream
-// through LDS 32 at a time.
+// dK/dV kernel of the backward: 4 wave64s (one per SIMD) x 64 keys = 256 keys per work item;
+// queries stream through LDS 32 at a time.
 constexpr int kDkvKeyTile = 256;
 constexpr int kDkvQueryStep = 32;
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;  // block size of the element-wise kernels (delta, fill, gather, scatter)
 constexpr int kNumXcd = 8;  // MI355X: 8 accelerator complex dies; workgroups go round-robin
 
 // One work item: a tile of rows of one stream and head, and the list of row ranges of the
