@@ -75,7 +75,25 @@ def token_valid(geom) -> np.ndarray:
     return v
 
 
-def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
+def _as_index(idx: np.ndarray):
+    """A run of consecutive indices as a slice (basic indexing, fast), any other set as is."""
+    if idx.size and int(idx[-1]) - int(idx[0]) + 1 == idx.size and np.all(np.diff(idx) == 1):
+        return slice(int(idx[0]), int(idx[-1]) + 1)
+    return idx
+
+
+def _put(M: np.ndarray, r: np.ndarray, c: np.ndarray, val) -> None:
+    """M[r x c] = val for row indices r and column indices c (val broadcasts to [len r, len c])."""
+    if r.size == 0 or c.size == 0:
+        return
+    rs, cs = _as_index(r), _as_index(c)
+    if isinstance(rs, slice) or isinstance(cs, slice):
+        M[rs, cs] = val
+    else:
+        M[np.ix_(rs, cs)] = val
+
+
+def visibility_mask(geom, rows: Optional[np.ndarray] = None, cols: Optional[np.ndarray] = None) -> np.ndarray:
     """Explicit visibility mask of one sample, rows and columns in [gen ; ref] order.
 
     M[q, k] is True when query q may attend to key k:
@@ -88,40 +106,33 @@ def visibility_mask(geom, rows: Optional[np.ndarray] = None) -> np.ndarray:
       ref q, ref k : valid(q) and valid(k) and group(q) == group(k)
     where valid(t) is the token validity of token_valid (its frame's, and its own entry of
     the token mask when there is one).
-    `rows` selects a subset of query rows (row-block mode for large shapes).
+    `rows` selects a subset of query rows and `cols` a subset of key columns (block mode for
+    large shapes); the result is [len(rows), len(cols)].
     """
     G, R, F = sample_sizes(geom)
     tv = token_valid(geom)
     g = int(geom.group_frames)
     assert g >= 1
-    if rows is None:
-        rows = np.arange(G + R)
-    rows = np.asarray(rows, dtype=np.int64)
-    M = np.zeros((rows.size, G + R), dtype=bool)
-    is_gen = rows < G
-    key_frame = np.arange(R) // F if F > 0 else np.zeros(0, dtype=np.int64)
-    key_valid = tv
-    key_group = key_frame // g
+    rows = np.arange(G + R) if rows is None else np.asarray(rows, dtype=np.int64)
+    cols = np.arange(G + R) if cols is None else np.asarray(cols, dtype=np.int64)
+    M = np.zeros((rows.size, cols.size), dtype=bool)
+    qg, qr = np.nonzero(rows < G)[0], np.nonzero(rows >= G)[0]   # gen / ref query rows
+    kg, kr = np.nonzero(cols < G)[0], np.nonzero(cols >= G)[0]   # gen / ref key columns
+    kref = cols[kr] - G                                          # reference token of each ref column
     # generation query rows
     w = getattr(geom, "gen_window", None)
     if w is None:
-        M[is_gen, :G] = True
+        _put(M, qg, kg, True)
     else:
         assert w >= 0
         Fg = geom.gen_h * geom.gen_w
-        q_gframe = rows[is_gen] // Fg
-        k_gframe = np.arange(G) // Fg
-        M[np.ix_(np.nonzero(is_gen)[0], np.arange(G))] = np.abs(q_gframe[:, None] - k_gframe[None, :]) <= w
-    M[np.ix_(is_gen, np.arange(G, G + R))] = key_valid[None, :]
-    # reference query rows
-    ref_rows = np.nonzero(~is_gen)[0]
-    if ref_rows.size:
-        j = rows[ref_rows] - G
-        q_frame = j // F
-        q_valid = tv[j]
-        q_group = q_frame // g
-        blk = q_valid[:, None] & key_valid[None, :] & (q_group[:, None] == key_group[None, :])
-        M[np.ix_(ref_rows, np.arange(G, G + R))] = blk
+        _put(M, qg, kg, np.abs((rows[qg] // Fg)[:, None] - (cols[kg] // Fg)[None, :]) <= w)
+    _put(M, qg, kr, tv[kref][None, :])
+    # reference query rows (no generation key is visible to them)
+    if qr.size and kr.size:
+        j = rows[qr] - G
+        same_group = ((j // F) // g)[:, None] == ((kref // F) // g)[None, :]
+        _put(M, qr, kr, tv[j][:, None] & tv[kref][None, :] & same_group)
     return M
 
 
@@ -321,19 +332,18 @@ def dkv_keys(x, samples, b: int, h: int, keys: np.ndarray, scale=None, dtype=np.
     kt = torch.from_numpy(keys)
     dk = torch.zeros((len(keys), d), dtype=tdt)
     dv = torch.zeros((len(keys), d), dtype=tdt)
-    for r0 in range(0, q.shape[0], block_rows):
-        rows = np.arange(r0, min(q.shape[0], r0 + block_rows))
-        M = visibility_mask(geom, rows)
-        sees = M[:, keys].any(axis=1)
-        if not sees.any():
-            continue
-        rows, M = torch.from_numpy(rows[sees]), torch.from_numpy(M[sees])
-        # masked softmax of the block's full rows (every row here sees at least one key)
+    # the query rows that see at least one of the keys (mask restricted to the key columns)
+    seers = np.concatenate([r0 + np.nonzero(visibility_mask(geom, np.arange(r0, min(q.shape[0], r0 + block_rows)),
+                                                              keys).any(axis=1))[0]
+                            for r0 in range(0, q.shape[0], block_rows)])
+    for i0 in range(0, seers.size, block_rows):
+        rows = seers[i0:i0 + block_rows]
+        M = torch.from_numpy(visibility_mask(geom, rows))
+        rows = torch.from_numpy(rows)
+        # masked softmax of the block's full rows (every row here sees at least one key):
+        # P = exp(S - rowmax) / rowsum, torch's softmax of the masked logits
         S = (q[rows] @ k.T) * scale
-        S = S.masked_fill(~M, float("-inf"))
-        m = S.amax(dim=1, keepdim=True)
-        E = torch.exp(S - m)
-        P = E / E.sum(dim=1, keepdim=True)
+        P = torch.softmax(S.masked_fill(~M, float("-inf")), dim=1)
         o = P @ v
         D = (do[rows] * o).sum(dim=1, keepdim=True)
         Pk = P[:, kt]
