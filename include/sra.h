@@ -24,7 +24,9 @@
  *             (token stride heads*head_dim). lse tensors are fp32 [heads, tokens], natural log.
  *   Memory    every data pointer and the workspace are DEVICE pointers owned by the caller.
  *             The library allocates no device memory. It owns pinned host staging buffers for
- *             its cached schedules (freed by sra_release_caches or at process exit).
+ *             its cached schedules (reused across plans, freed by sra_release_caches or at
+ *             process exit); a geometry not seen before costs one host planning pass and, when
+ *             no staging buffer is free, one hipHostMalloc (the cache holds 256 plans).
  *   Streams   `stream` is a hipStream_t (NULL = the default stream). Calls only enqueue work
  *             on it and never synchronise the device.
  *   Errors    every argument is validated before anything is enqueued, so a call that
@@ -33,8 +35,9 @@
  *   Supported head_dim in {64, 128}; heads >= 1; batch >= 1; every sample has >= 1 gen token.
  *   Limits    packed tokens of each stream <= 2^31 - 1 (beyond: SRA_ERR_INVALID_ARGUMENT);
  *             num_heads * packed tokens of each stream <= 2^31 - 1 (beyond: SRA_ERR_UNSUPPORTED;
- *             per-row statistics are indexed in 32 bits). Tensors themselves may exceed 2^31
- *             elements: token offsets are 64-bit.
+ *             per-row statistics are indexed in 32 bits); token strides <= (2^31 - 1) / 64
+ *             elements (beyond: SRA_ERR_UNSUPPORTED; offsets inside a tile are 32-bit). Tensors
+ *             themselves may exceed 2^31 elements: token offsets are 64-bit.
  */
 #ifndef SRA_H_
 #define SRA_H_
@@ -121,7 +124,10 @@ sra_status sra_forward(const sra_problem* p,
                        void* o_gen, void* o_ref, float* lse_gen, float* lse_ref,
                        void* workspace, size_t workspace_bytes, void* stream);
 
-/* Backward pass: gradients of the forward outputs o_gen/o_ref with respect to every input,
+/* Backward pass (§3.3: personality SFT trains the model with Sparse Reference Attention in the
+ * loop, so the method needs the gradient of the attention of the top of this file; it is the
+ * gradient of masked softmax attention, which the paper does not spell out).
+ * Gradients of the forward outputs o_gen/o_ref with respect to every input,
  * given the upstream gradients do_gen/do_ref (bf16, dense, same shapes as o) and the forward's
  * o and lse (as sra_forward wrote them). Writes dq/dk/dv for both streams (bf16, dense,
  * same shapes as q/k/v); it overwrites them and does not accumulate. Gradients of tokens of
@@ -140,24 +146,36 @@ sra_status sra_backward(const sra_problem* p,
 
 /* ---- host-only inspection hooks (no device needed; used to test the schedules) ---------- */
 
-/* Visible (query, key) pairs per head summed over samples, from the closed form
+/* Visible (query, key) pairs per head summed over samples: the work of the attention, which
+ * §1 and §2.1 state grows (almost) linearly with the reference length; from the closed form
  * G*(G + R_valid) for gen queries (G*R_valid plus the window's gen pairs with
  * SRA_FLAG_GEN_WINDOW) and sum over groups of (valid tokens of the group)^2 for ref queries.
  * Either output pointer may be NULL. */
 sra_status sra_pair_counts(const sra_problem* p, int64_t* gen_pairs, int64_t* ref_pairs);
 
-/* Sizes of schedule `which` (SRA_SCHED_*): work items (all heads) and span entries, and the
+/* The visibility rule of the top of this file (§1, §2.1, §4.3; the window of §2.4 with
+ * SRA_FLAG_GEN_WINDOW) written out for `sample` as a (G+R) x (G+R) byte matrix, rows = queries
+ * and columns = keys in [gen ; ref] order of that sample: out[q*(G+R)+k] = 1 when query q sees
+ * key k, else 0. Computed from the geometry alone (not from a schedule; sra_schedule_mask
+ * gives what a schedule covers). Other flags do not change it. out must hold (G+R)^2 bytes
+ * (host memory owned by the caller); host only. */
+sra_status sra_dense_mask(const sra_problem* p, int32_t sample, uint8_t* out);
+
+/* Sizes of schedule `which` (SRA_SCHED_*), the tile schedules that realise the visibility rule
+ * of §1, §2.1 and §4.3 without a dense mask: work items (all heads) and span entries, and the
  * (query, key) pairs the schedule covers per head (must equal the pair count). */
 sra_status sra_schedule_info(const sra_problem* p, int which, int64_t* n_items,
                              int64_t* n_spans, int64_t* covered_pairs);
 
-/* Expands schedule `which` for head 0 of `sample` into a (G+R) x (G+R) byte matrix, rows =
+/* Expands schedule `which` (the visibility rule of §1, §2.1 and §4.3 as tiles) for head 0 of
+ * `sample` into a (G+R) x (G+R) byte matrix, rows =
  * queries and columns = keys in [gen ; ref] order of that sample: out[q*(G+R)+k] = number of
  * work items that compute the pair (q, k), so a correct schedule gives exactly the 0/1
  * visibility mask. out must hold (G+R)^2 bytes (host). */
 sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, uint8_t* out);
 
-/* Copies schedule `which` into host buffers: items[8*i + 0..7] = {stream, head, start, length,
+/* Copies schedule `which` (the tiles realising §1, §2.1 and §4.3) into host buffers:
+ * items[8*i + 0..7] = {stream, head, start, length,
  * span_offset, span_count, sample, reserved} per work item, spans[4*j + 0..3] = {stream,
  * start, length, keys} per span (stream 0 = gen, 1 = ref; start = packed token row; keys, in
  * the dK/dV schedule only: the item's keys [lo, hi), counted from its first key, that the
@@ -171,7 +189,7 @@ sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, ui
 sra_status sra_schedule_export(const sra_problem* p, int which, int32_t* items,
                                int64_t items_capacity, int32_t* spans, int64_t spans_capacity);
 
-/* ---- per-kernel timing (tracing hook) ---------------------------------------------------- */
+/* ---- per-kernel timing (tracing hook; library infrastructure, no passage of the paper) --- */
 
 /* Kernels of the library, for sra_kernel_timing. */
 enum {
@@ -193,13 +211,18 @@ sra_status sra_kernel_timing_enable(int enable);
  * kernel `kernel` (SRA_KERNEL_*) since timing was enabled. */
 sra_status sra_kernel_timing(int kernel, double* total_ms, int64_t* launches);
 
-/* Frees cached schedules and their pinned host buffers, after waiting for the copies that
- * read them. Safe to call at any time; later calls rebuild what they need. */
+/* Library infrastructure (no passage of the paper). Frees cached schedules and their pinned
+ * host staging buffers, after waiting for the copies that read them (the only entry point that
+ * waits on the device). Evicting a plan from the cache neither waits nor frees: its staging
+ * buffer is reused for a later plan once the copies out of it have completed. Safe to call at
+ * any time; later calls rebuild what they need. */
 sra_status sra_release_caches(void);
 
+/* Library infrastructure (no passage of the paper): status names, the per-thread detail of
+ * the last failing call ("" if none), and the version as major*10000 + minor*100 + patch. */
 const char* sra_status_string(sra_status s);
-const char* sra_last_error(void);   /* per-thread detail of the last failing call ("" if none) */
-int32_t sra_version(void);          /* major*10000 + minor*100 + patch                         */
+const char* sra_last_error(void);
+int32_t sra_version(void);
 
 #ifdef __cplusplus
 }

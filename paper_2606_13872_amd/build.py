@@ -71,6 +71,48 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host-only build for the sanitizer run: the scheduler and the C ABI compiled with g++ under
+# AddressSanitizer and UndefinedBehaviorSanitizer, the kernel launchers replaced by stubs that
+# report hipErrorNotSupported. No device code is built. The tests of the schedules and of the
+# ABI's host validation load it through SRA_HOST_LIB, with libasan preloaded into Python:
+#   python -m paper_2606_13872_amd.build --sanitize
+#   SRA_HOST_LIB=paper_2606_13872_amd/_build/sanitize/libsra_host.so \
+#   LD_PRELOAD=$(g++ -print-file-name=libasan.so) ASAN_OPTIONS=detect_leaks=0 \
+#   UBSAN_OPTIONS=halt_on_error=1:print_stacktrace=1 python -m pytest tests/test_schedule.py tests/test_abi.py
+SAN_DIR = os.path.join(BUILD, "sanitize")
+SAN_LIB = os.path.join(SAN_DIR, "libsra_host.so")
+SAN_SOURCES = ["schedule.cpp", "sra_api.cpp", "sra_host_stubs.cpp"]
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer", "-g",
+             "-O1"]
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    os.makedirs(SAN_DIR, exist_ok=True)
+    # g++ 11 has no __bf16; the host code only passes bf16 tensors around as pointers
+    hip = ["-D__HIP_PLATFORM_AMD__", "-D__bf16=uint16_t", "-I", os.path.join(ROCM, "include")]
+    flags = [f for f in COMMON if f != "-O3"]
+    objs = []
+    for src in SAN_SOURCES:
+        obj = os.path.join(SAN_DIR, os.path.splitext(src)[0] + ".o")
+        cmd = ["g++", *flags, *hip, *SAN_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True, timeout=COMPILE_TIMEOUT_S)
+        if r.returncode != 0:
+            raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+        objs.append(obj)
+    cmd = ["g++", "-shared", *SAN_FLAGS, "-o", SAN_LIB, *objs, "-L", os.path.join(ROCM, "lib"), "-lamdhip64",
+           f"-Wl,-rpath,{os.path.join(ROCM, 'lib')}"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    if verbose:
+        print("built", SAN_LIB)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
-    build(verbose=True)
+    if "--sanitize" in sys.argv[1:]:
+        build_sanitized(verbose=True)
+    else:
+        build(verbose=True)
     sys.exit(0)

@@ -82,6 +82,12 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
     return SRA_ERR_INVALID_ARGUMENT;
   }
   const int64_t kRowLimit = (int64_t(1) << 31) - 1;
+  // The kernels' tile loaders hold the offset of a row inside a tile (up to 63 rows past the
+  // tile's first row, plus the head's columns) in 32 bits.
+  if (L.gen_stride > kRowLimit / 64 || L.ref_stride > kRowLimit / 64) {
+    *err = "token stride exceeds (2^31 - 1) / 64 elements (32-bit offsets inside a tile)";
+    return SRA_ERR_UNSUPPORTED;
+  }
   L.samples.resize(p->batch);
   for (int32_t b = 0; b < p->batch; ++b) {
     const sra_sample_geom& g = p->samples[b];

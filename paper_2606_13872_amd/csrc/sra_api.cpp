@@ -28,26 +28,31 @@ sra_status fail(sra_status s, const std::string& msg) {
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Pinned host staging buffer for uploading a plan's tables, with the events recorded after the
+// copies enqueued out of it. A buffer is reused for another plan once every such copy has run
+// (checked with hipEventQuery, never by waiting), so evicting a plan neither synchronises nor
+// frees anything; buffers are freed only by sra_release_caches.
+struct Staging {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+  const void* owner = nullptr;     // the Blob whose image the buffer holds (nullptr = retired)
+  std::vector<hipEvent_t> pending; // one per enqueued copy not yet known to be complete
+};
+
 // Byte image of a set of tables, laid out back to back (each 256-byte aligned). The pinned
-// copy is made on first use by a launch, so sizes can be queried without a device.
+// copy is made on first upload, so sizes can be queried without a device.
 struct Blob {
   std::vector<size_t> offsets;
   std::vector<char> image;
   size_t bytes = 0;
-  void* pinned = nullptr;  // hipHostMalloc'd copy of the image
+  Staging* stage = nullptr;        // owned by the plan cache; valid while stage->owner == this
 };
 
 struct CachedPlan {
   Plan plan;
+  uint64_t id = 0;  // unique per plan built by this process
   Blob fwd;   // fwd items | fwd spans | fill | ref gather | ref scatter
   Blob bwd;   // dq items | dq spans | dkv items | dkv spans | fill | ref gather | ref scatter
-  // Runs when the cache has dropped the plan and no call holds it any more. An upload
-  // enqueued by an earlier call may still read the pinned images: wait for the device.
-  ~CachedPlan() {
-    if (fwd.pinned || bwd.pinned) (void)hipDeviceSynchronize();
-    if (fwd.pinned) (void)hipHostFree(fwd.pinned);
-    if (bwd.pinned) (void)hipHostFree(bwd.pinned);
-  }
 };
 
 template <class T>
@@ -73,6 +78,7 @@ class PlanCache {
     }
     auto cp = std::make_shared<CachedPlan>();
     build_plan(L, &cp->plan);
+    cp->id = ++next_id_;
     put_table(cp->fwd, cp->plan.fwd.items);
     put_table(cp->fwd, cp->plan.fwd.spans);
     put_table(cp->fwd, cp->plan.fill);
@@ -92,37 +98,117 @@ class PlanCache {
     return SRA_OK;
   }
 
-  // Pinned staging copy of a blob, made once per plan (the image never changes afterwards).
-  sra_status pinned(Blob& b, void** out) {
+  // Enqueues the copy of blob `b` into device memory `dst` on `s` (from its pinned staging
+  // buffer, filled on first use) and records an event after it.
+  sra_status upload(Blob& b, void* dst, hipStream_t s) {
+    if (!b.bytes) return SRA_OK;
     std::lock_guard<std::mutex> lk(mu_);
-    if (!b.pinned && b.bytes) {
+    if (!b.stage || b.stage->owner != &b) {
+      sra_status st = acquire(b);
+      if (st != SRA_OK) return st;
+    }
+    Staging& g = *b.stage;
+    hipError_t e = hipMemcpyAsync(dst, g.ptr, b.bytes, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return fail(SRA_ERR_HIP, std::string("schedule upload: ") + hipGetErrorString(e));
+    hipEvent_t ev = nullptr;
+    if (!free_events_.empty()) {
+      ev = free_events_.back();
+      free_events_.pop_back();
+    } else if ((e = hipEventCreateWithFlags(&ev, hipEventDisableTiming)) != hipSuccess) {
+      return fail(SRA_ERR_HIP, std::string("event for the schedule upload: ") + hipGetErrorString(e));
+    }
+    if ((e = hipEventRecord(ev, s)) != hipSuccess) {
+      free_events_.push_back(ev);
+      return fail(SRA_ERR_HIP, std::string("event after the schedule upload: ") + hipGetErrorString(e));
+    }
+    g.pending.push_back(ev);
+    return SRA_OK;
+  }
+
+  // Waits for every upload, then frees the staging buffers and drops every plan (calls still
+  // holding a plan re-stage its image on their next upload).
+  void clear() {
+    std::lock_guard<std::mutex> lk(mu_);
+    for (auto& g : stagings_) {
+      for (hipEvent_t ev : g->pending) {
+        (void)hipEventSynchronize(ev);
+        (void)hipEventDestroy(ev);
+      }
+      if (g->ptr) (void)hipHostFree(g->ptr);
+    }
+    stagings_.clear();
+    for (hipEvent_t ev : free_events_) (void)hipEventDestroy(ev);
+    free_events_.clear();
+    map_.clear();
+    lru_.clear();
+  }
+
+  size_t staging_buffers() {
+    std::lock_guard<std::mutex> lk(mu_);
+    return stagings_.size();
+  }
+
+ private:
+  static constexpr size_t kMaxPlans = 256;
+
+  // Moves the completed events of `g` to the free list; true when none is pending.
+  bool reap(Staging& g) {
+    size_t keep = 0;
+    bool not_ready = false;
+    for (hipEvent_t ev : g.pending) {
+      const hipError_t q = hipEventQuery(ev);
+      if (q == hipSuccess) {
+        free_events_.push_back(ev);
+      } else {
+        g.pending[keep++] = ev;
+        not_ready |= q == hipErrorNotReady;
+      }
+    }
+    g.pending.resize(keep);
+    if (not_ready) (void)hipGetLastError();  // a copy still running is not an error of any call
+    return keep == 0;
+  }
+
+  // Gives blob `b` a staging buffer holding its image: a retired one that is large enough and
+  // no longer read by any copy, else a new pinned allocation.
+  sra_status acquire(Blob& b) {
+    Staging* pick = nullptr;
+    for (auto& g : stagings_)
+      if (!g->owner && g->bytes >= b.bytes && reap(*g) && (!pick || g->bytes < pick->bytes)) pick = g.get();
+    if (!pick) {
       void* p = nullptr;
       if (hipHostMalloc(&p, b.bytes, hipHostMallocDefault) != hipSuccess) {
         (void)hipGetLastError();
         return fail(SRA_ERR_HIP, "hipHostMalloc of schedule staging failed");
       }
-      std::memcpy(p, b.image.data(), b.image.size());
-      b.pinned = p;
+      stagings_.push_back(std::make_unique<Staging>());
+      pick = stagings_.back().get();
+      pick->ptr = p;
+      pick->bytes = b.bytes;
     }
-    *out = b.pinned;
+    std::memcpy(pick->ptr, b.image.data(), b.image.size());
+    pick->owner = &b;
+    b.stage = pick;
     return SRA_OK;
   }
 
-  void clear() {
-    std::lock_guard<std::mutex> lk(mu_);
-    map_.clear();
-    lru_.clear();
+  void retire(Blob& b) {
+    if (b.stage && b.stage->owner == &b) b.stage->owner = nullptr;
   }
 
- private:
-  static constexpr size_t kMaxPlans = 256;
   void evict_one() {
-    map_.erase(lru_.back());
+    auto it = map_.find(lru_.back());
+    retire(it->second.first->fwd);
+    retire(it->second.first->bwd);
+    map_.erase(it);
     lru_.pop_back();
   }
   std::mutex mu_;
   std::list<std::string> lru_;
   std::unordered_map<std::string, std::pair<std::shared_ptr<CachedPlan>, std::list<std::string>::iterator>> map_;
+  std::vector<std::unique_ptr<Staging>> stagings_;
+  std::vector<hipEvent_t> free_events_;
+  uint64_t next_id_ = 0;
 };
 
 PlanCache& cache() {
@@ -294,13 +380,8 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
-  {
-    void* src = nullptr;
-    st = cache().pinned(cp->fwd, &src);
-    if (st != SRA_OK) return st;
-    hipError_t e = hipMemcpyAsync(ws, src, cp->fwd.bytes, hipMemcpyHostToDevice, s);
-    if (e != hipSuccess) return hip_fail(e, "schedule upload");
-  }
+  st = cache().upload(cp->fwd, ws, s);
+  if (st != SRA_OK) return st;
   const Plan& P = cp->plan;
   const Layout& E = P.exec;
   const int32_t row_elems = L.heads * L.head_dim;
@@ -408,11 +489,9 @@ sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_g
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
-  void* src = nullptr;
-  st = cache().pinned(cp->bwd, &src);
+  st = cache().upload(cp->bwd, ws, s);
   if (st != SRA_OK) return st;
-  hipError_t e = hipMemcpyAsync(ws, src, cp->bwd.bytes, hipMemcpyHostToDevice, s);
-  if (e != hipSuccess) return hip_fail(e, "schedule upload");
+  hipError_t e;
   const Plan& P = cp->plan;
   const Layout& E = P.exec;
   const int32_t row_elems = L.heads * L.head_dim;
@@ -546,6 +625,37 @@ sra_status sra_pair_counts(const sra_problem* p, int64_t* gen_pairs, int64_t* re
   sra_status st = make_layout(p, &L, &err);
   if (st != SRA_OK) return fail(st, err);
   closed_form_pairs(L, gen_pairs, ref_pairs);
+  return SRA_OK;
+}
+
+sra_status sra_dense_mask(const sra_problem* p, int32_t sample, uint8_t* out) {
+  g_last_error.clear();
+  Layout L;
+  std::string err;
+  sra_status st = make_layout(p, &L, &err);
+  if (st != SRA_OK) return fail(st, err);
+  if (sample < 0 || sample >= L.batch) return fail(SRA_ERR_INVALID_ARGUMENT, "sample out of range");
+  if (!out) return fail(SRA_ERR_INVALID_ARGUMENT, "out is NULL");
+  const SampleLayout& sm = L.samples[sample];
+  const int64_t G = sm.G, R = sm.R, n = G + R;
+  std::vector<uint8_t> valid(size_t(R), 0);  // reference token takes part (its frame and its own entry)
+  for (const auto& r : sm.vruns)
+    for (int64_t j = r.first; j < r.second; ++j) valid[size_t(j)] = 1;
+  const int64_t gsz = sm.F * sm.group;  // reference tokens per self-attention group
+  for (int64_t q = 0; q < n; ++q) {
+    uint8_t* row = out + q * n;
+    if (q < G) {  // generation query: gen keys (within the window, if any), every valid ref key
+      for (int64_t k = 0; k < G; ++k)
+        row[k] = sm.window < 0 || std::llabs(q / sm.Fg - k / sm.Fg) <= sm.window;
+      for (int64_t j = 0; j < R; ++j) row[G + j] = valid[size_t(j)];
+    } else {  // reference query: no gen key; the valid ref keys of its own group if it is valid
+      const int64_t i = q - G;
+      std::memset(row, 0, size_t(n));
+      if (!valid[size_t(i)]) continue;
+      const int64_t g0 = i / gsz * gsz, g1 = std::min(R, g0 + gsz);
+      for (int64_t j = g0; j < g1; ++j) row[G + j] = valid[size_t(j)];
+    }
+  }
   return SRA_OK;
 }
 

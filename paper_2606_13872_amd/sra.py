@@ -58,13 +58,18 @@ _lib_handle = None
 
 
 def lib() -> ctypes.CDLL:
-    """Loads libsra.so from this package directory (raises if it was not built)."""
+    """Loads libsra.so from this package directory (raises if it was not built).
+
+    SRA_HOST_LIB names another build of the library to load instead: the host-only build of
+    `build.py --sanitize` (scheduler and C ABI under AddressSanitizer and UBSan, no kernels),
+    for the sanitizer run of the host tests. Its launches all fail with SRA_ERR_HIP."""
     global _lib_handle
     if _lib_handle is not None:
         return _lib_handle
-    if not os.path.exists(LIB_PATH):
-        raise ImportError(f"libsra.so is not built ({LIB_PATH}); run `python -m paper_2606_13872_amd.build`")
-    L = ctypes.CDLL(LIB_PATH)
+    path = os.environ.get("SRA_HOST_LIB") or LIB_PATH
+    if not os.path.exists(path):
+        raise ImportError(f"libsra.so is not built ({path}); run `python -m paper_2606_13872_amd.build`")
+    L = ctypes.CDLL(path)
     P = ctypes.POINTER(_Problem)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     sig = {
@@ -74,6 +79,7 @@ def lib() -> ctypes.CDLL:
         "sra_pair_counts": [P, ctypes.POINTER(i64), ctypes.POINTER(i64)],
         "sra_schedule_info": [P, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)],
         "sra_schedule_mask": [P, ctypes.c_int, i32, vp],
+        "sra_dense_mask": [P, i32, vp],
         "sra_schedule_export": [P, ctypes.c_int, vp, i64, vp, i64],
         "sra_release_caches": [],
         "sra_kernel_timing_enable": [ctypes.c_int],
@@ -159,6 +165,35 @@ class Problem:
         return int(n.value)
 
 
+_PROBLEMS: "OrderedDict" = None
+
+
+def _problem(samples, heads, head_dim, scale, gen_stride, ref_stride, flags) -> Problem:
+    """Problem(...), reused across calls with the same geometry (samples are frozen, so a tuple of
+    them is a key when their masks are tuples); built afresh when they cannot be hashed."""
+    global _PROBLEMS
+    from collections import OrderedDict
+
+    if _PROBLEMS is None:
+        _PROBLEMS = OrderedDict()
+    frozen = all(getattr(getattr(g, "__dataclass_params__", None), "frozen", False) for g in samples)
+    try:
+        if not frozen:  # geometry objects that may change between calls are never cached
+            raise TypeError
+        key = (tuple(samples), heads, head_dim, scale, gen_stride, ref_stride, flags)
+        hit = _PROBLEMS.get(key)
+    except TypeError:  # mutable geometry, or a mask given as a list or an array
+        return Problem(samples, heads, head_dim, scale, gen_stride, ref_stride, flags)
+    if hit is None:
+        hit = Problem(samples, heads, head_dim, scale, gen_stride, ref_stride, flags)
+        _PROBLEMS[key] = hit
+        if len(_PROBLEMS) > 64:
+            _PROBLEMS.popitem(last=False)
+    else:
+        _PROBLEMS.move_to_end(key)
+    return hit
+
+
 # ----------------------------------------------------------------------------- host hooks
 def pair_counts(samples, heads=1, head_dim=128, flags=0) -> Tuple[int, int]:
     p = Problem(samples, heads, head_dim, flags=flags)
@@ -182,6 +217,18 @@ def schedule_mask(samples, which: int, sample: int, heads=1, head_dim=128, flags
     n = g.gen_frames * g.gen_h * g.gen_w + g.ref_frames * g.ref_h * g.ref_w
     out = np.zeros((n, n), dtype=np.uint8)
     _check(lib().sra_schedule_mask(p.ptr, which, sample, out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def dense_mask(samples, sample: int, heads=1, head_dim=128, flags=0):
+    """sra_dense_mask: the visibility rule of `sample` as a (G+R) x (G+R) uint8 matrix."""
+    p = Problem(samples, heads, head_dim, flags=flags)
+    if not 0 <= sample < len(p.samples):  # the library rejects it too; no buffer to size here
+        _check(lib().sra_dense_mask(p.ptr, sample, None))
+    g = p.samples[sample]
+    n = g.gen_frames * g.gen_h * g.gen_w + g.ref_frames * g.ref_h * g.ref_w
+    out = np.zeros((n, n), dtype=np.uint8)
+    _check(lib().sra_dense_mask(p.ptr, sample, out.ctypes.data_as(ctypes.c_void_p)))
     return out
 
 
@@ -268,54 +315,147 @@ def _check_cu_seqlens(samples, cu_gen, cu_ref):
             raise SRAError(SRA_ERR_INVALID_ARGUMENT, f"{name} {a.tolist()} does not match the geometry {w.tolist()}")
 
 
+def _bad(msg):
+    return SRAError(SRA_ERR_INVALID_ARGUMENT, msg)
+
+
+_torch = None
+
+
+def _tm():
+    """torch, imported on first use (the host-only hooks of this module do not need it)."""
+    global _torch
+    if _torch is None:
+        import torch
+        _torch = torch
+    return _torch
+
+
+def _expect(t, name, shape, dtype, dense):
+    """Checks one tensor argument: dtype, exact shape and (dense) row-major layout. The q/k/v
+    inputs (dense=False) need contiguous heads only; their token stride is checked separately."""
+    if not isinstance(t, _tm().Tensor):
+        raise _bad(f"{name} must be a torch tensor, got {type(t).__name__}")
+    if t.dtype != dtype:
+        raise _bad(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if t.shape != shape:
+        raise _bad(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if dense:
+        if not t.is_contiguous():
+            raise _bad(f"{name} must be dense (contiguous)")
+    elif t.numel() and (t.stride(2) != 1 or (shape[1] > 1 and t.stride(1) != shape[2])):
+        raise _bad(f"{name} must be [tokens, heads, head_dim] with contiguous heads")
+
+
+def _same_device(tensors, device):
+    """Every tensor of the (name, tensor) pairs must live on `device`, a GPU."""
+    if device.type != "cuda":
+        raise _bad(f"tensors must be on a GPU (HIP device), got {device}")
+    idx = device.index
+    for name, t in tensors:
+        if t is not None and (not t.is_cuda or t.get_device() != idx):
+            raise _bad(f"{name} is on {t.device}, q_gen on {device}")
+
+
+def _inputs(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, gen_only):
+    """Validates q/k/v of both streams against the geometry; returns (H, d, n_gen, n_ref)."""
+    torch = _tm()
+    if not isinstance(q_gen, torch.Tensor) or q_gen.dim() != 3:
+        raise _bad("q_gen must be a [tokens, heads, head_dim] tensor")
+    H, d = int(q_gen.shape[1]), int(q_gen.shape[2])
+    n_gen = sum(s.gen_frames * s.gen_h * s.gen_w for s in samples)
+    n_ref = sum(s.ref_frames * s.ref_h * s.ref_w for s in samples)
+    bf = torch.bfloat16
+    sg, sr = (n_gen, H, d), (n_ref, H, d)
+    _expect(q_gen, "q_gen", sg, bf, False)
+    _expect(k_gen, "k_gen", sg, bf, False)
+    _expect(v_gen, "v_gen", sg, bf, False)
+    for name, t in (("q_ref", q_ref), ("k_ref", k_ref), ("v_ref", v_ref)):
+        if t is None and (n_ref == 0 or (gen_only and name == "q_ref")):
+            continue
+        _expect(t, name, sr, bf, False)
+    return H, d, n_gen, n_ref
+
+
 def _out(out, name, shape, dtype, device):
-    """The caller's output buffer `name`, or a new one (allocated only when none was given)."""
-    import torch
-
+    """The caller's output buffer `name` (checked: dtype, shape, dense, device), or a new one
+    (allocated only when none was given)."""
     t = out.get(name)
-    return torch.empty(shape, dtype=dtype, device=device) if t is None else t
+    if t is None:
+        return _tm().empty(shape, dtype=dtype, device=device)
+    _expect(t, name, shape, dtype, True)
+    _same_device(((name, t),), device)
+    return t
 
 
-def _alloc_workspace(nbytes, device):
+def _precheck_outs(out, specs):
+    """dtype, shape and layout of the caller's output buffers, before any device check."""
+    for name, shape, dtype in specs:
+        t = (out or {}).get(name)
+        if t is not None:
+            _expect(t, name, shape, dtype, True)
+
+
+def _workspace(out, nbytes, device):
+    """The caller's workspace (a uint8 tensor on the device, used when large enough) or a new one."""
     import torch
 
+    ws = out.get("workspace")
+    if ws is not None:
+        if not isinstance(ws, torch.Tensor) or ws.dtype != torch.uint8 or not ws.is_contiguous():
+            raise _bad("workspace must be a contiguous uint8 tensor")
+        _same_device((("workspace", ws),), device)
+        if ws.numel() >= nbytes:
+            return ws
     return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+def _forward_args(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale, out, gen_queries_only,
+                  cu_seqlens_gen, cu_seqlens_ref):
+    """Checks the forward's arguments and builds the problem and the output tensors."""
+    import torch
+
+    _check_cu_seqlens(samples, cu_seqlens_gen, cu_seqlens_ref)
+    go = bool(gen_queries_only)
+    if go:
+        q_ref = None
+    H, d, n_gen, n_ref = _inputs(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, go)
+    _precheck_outs(out, [("o_gen", (n_gen, H, d), torch.bfloat16), ("lse_gen", (H, n_gen), torch.float32)] +
+                   ([] if go else [("o_ref", (n_ref, H, d), torch.bfloat16), ("lse_ref", (H, n_ref), torch.float32)]))
+    dev = q_gen.device
+    _same_device((("q_gen", q_gen), ("k_gen", k_gen), ("v_gen", v_gen), ("q_ref", q_ref), ("k_ref", k_ref),
+                  ("v_ref", v_ref)), dev)
+    p = _problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
+                 _token_stride([q_ref, k_ref, v_ref], "ref"), FLAG_GEN_QUERIES_ONLY if go else 0)
+    out = out or {}
+    o_gen = _out(out, "o_gen", (n_gen, H, d), torch.bfloat16, dev)
+    lse_gen = _out(out, "lse_gen", (H, n_gen), torch.float32, dev)
+    if go:
+        o_ref = lse_ref = None
+    else:
+        o_ref = _out(out, "o_ref", (n_ref, H, d), torch.bfloat16, dev)
+        lse_ref = _out(out, "lse_ref", (H, n_ref), torch.float32, dev)
+    return p, q_ref, o_gen, o_ref, lse_gen, lse_ref, out, dev
 
 
 def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[float] = None,
             out: Optional[Dict] = None, gen_queries_only: bool = False, cu_seqlens_gen=None, cu_seqlens_ref=None):
     """SRA forward on the GPU. Returns (o_gen, o_ref, lse_gen, lse_ref).
 
+    Inputs are bf16 [tokens, heads, head_dim] with contiguous heads (q, k and v of a stream
+    share one token stride). `out` may hold caller buffers o_gen, o_ref (bf16, dense), lse_gen,
+    lse_ref (fp32 [heads, tokens], dense) and workspace (uint8); every tensor must be on
+    q_gen's GPU. A wrong dtype, shape, layout or device raises SRAError
+    (SRA_ERR_INVALID_ARGUMENT) before anything reaches the library.
     gen_queries_only: the reference tokens are context only (cached reference K/V); only the
     generation rows are computed, q_ref may be None and o_ref / lse_ref are returned as None.
     cu_seqlens_gen / cu_seqlens_ref: optional packed-row offsets of the samples; they are
     checked against the geometry (SRAError with SRA_ERR_INVALID_ARGUMENT on a mismatch).
     """
-    import torch
-
-    _check_cu_seqlens(samples, cu_seqlens_gen, cu_seqlens_ref)
-    H, d = q_gen.shape[1], q_gen.shape[2]
-    dev = q_gen.device
-    go = bool(gen_queries_only)
-    p = Problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
-                _token_stride([None if go else q_ref, k_ref, v_ref], "ref"), FLAG_GEN_QUERIES_ONLY if go else 0)
-    for t in (q_gen, k_gen, v_gen, q_ref, k_ref, v_ref):
-        if t is not None and t.dtype != torch.bfloat16:
-            raise TypeError("q/k/v must be bfloat16")
-    if q_gen.shape[0] != p.n_gen or (k_ref is not None and k_ref.shape[0] != p.n_ref):
-        raise ValueError("token counts do not match the geometry")
-    out = out or {}
-    o_gen = _out(out, "o_gen", (p.n_gen, H, d), torch.bfloat16, dev)
-    lse_gen = _out(out, "lse_gen", (H, p.n_gen), torch.float32, dev)
-    if go:
-        q_ref = o_ref = lse_ref = None
-    else:
-        o_ref = _out(out, "o_ref", (p.n_ref, H, d), torch.bfloat16, dev)
-        lse_ref = _out(out, "lse_ref", (H, p.n_ref), torch.float32, dev)
-    nbytes = p.workspace_size(False)
-    ws = out.get("workspace")
-    if ws is None or ws.numel() < nbytes:
-        ws = _alloc_workspace(nbytes, dev)
+    p, q_ref, o_gen, o_ref, lse_gen, lse_ref, out, dev = _forward_args(
+        q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale, out, gen_queries_only, cu_seqlens_gen,
+        cu_seqlens_ref)
+    ws = _workspace(out, p.workspace_size(False), dev)
     _check(lib().sra_forward(p.ptr, _ptr(q_gen), _ptr(k_gen), _ptr(v_gen), _ptr(q_ref), _ptr(k_ref),
                              _ptr(v_ref), _ptr(o_gen), _ptr(o_ref), _ptr(lse_gen), _ptr(lse_ref),
                              _ptr(ws), ctypes.c_size_t(ws.numel()), _stream_ptr(dev)))
@@ -327,6 +467,9 @@ def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, ls
              cu_seqlens_gen=None, cu_seqlens_ref=None):
     """SRA backward on the GPU. Returns dict dq_gen, dk_gen, dv_gen, dq_ref, dk_ref, dv_ref.
 
+    q/k/v as for forward; o and do are bf16 [tokens, heads, head_dim] and lse fp32
+    [heads, tokens], all dense. `out` may hold caller buffers for the six gradients (bf16,
+    dense) and the workspace; every tensor must be on q_gen's GPU (SRAError otherwise).
     gen_queries_only: gradients of the generation rows alone (reference tokens are context
     only); q_ref, o_ref, lse_ref and do_ref may be None and dq_ref is returned as None.
     cu_seqlens_gen / cu_seqlens_ref: as for forward.
@@ -334,27 +477,36 @@ def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, ls
     import torch
 
     _check_cu_seqlens(samples, cu_seqlens_gen, cu_seqlens_ref)
-    H, d = q_gen.shape[1], q_gen.shape[2]
-    dev = q_gen.device
     go = bool(gen_queries_only)
     if go:
         q_ref = o_ref = lse_ref = do_ref = None
-    p = Problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
-                _token_stride([q_ref, k_ref, v_ref], "ref"), FLAG_GEN_QUERIES_ONLY if go else 0)
-    for t in (o_gen, o_ref, do_gen, do_ref):
-        if t is not None and t.numel() and not t.is_contiguous():
-            raise ValueError("o and do must be dense [tokens, heads, head_dim]")
+    H, d, n_gen, n_ref = _inputs(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, go)
+    _expect(o_gen, "o_gen", (n_gen, H, d), torch.bfloat16, True)
+    _expect(do_gen, "do_gen", (n_gen, H, d), torch.bfloat16, True)
+    _expect(lse_gen, "lse_gen", (H, n_gen), torch.float32, True)
+    if not go:
+        for name, t, shape, dt in (("o_ref", o_ref, (n_ref, H, d), torch.bfloat16),
+                                   ("do_ref", do_ref, (n_ref, H, d), torch.bfloat16),
+                                   ("lse_ref", lse_ref, (H, n_ref), torch.float32)):
+            if t is None and n_ref == 0:
+                continue
+            _expect(t, name, shape, dt, True)
+    _precheck_outs(out, [(n, (n_gen, H, d), torch.bfloat16) for n in ("dq_gen", "dk_gen", "dv_gen")] +
+                   [(n, (n_ref, H, d), torch.bfloat16) for n in ("dq_ref", "dk_ref", "dv_ref")
+                    if not (go and n == "dq_ref")])
+    dev = q_gen.device
+    _same_device((("q_gen", q_gen), ("k_gen", k_gen), ("v_gen", v_gen), ("q_ref", q_ref), ("k_ref", k_ref),
+                  ("v_ref", v_ref), ("o_gen", o_gen), ("o_ref", o_ref), ("lse_gen", lse_gen), ("lse_ref", lse_ref),
+                  ("do_gen", do_gen), ("do_ref", do_ref)), dev)
+    p = _problem(samples, H, d, scale, _token_stride([q_gen, k_gen, v_gen], "gen"),
+                 _token_stride([q_ref, k_ref, v_ref], "ref"), FLAG_GEN_QUERIES_ONLY if go else 0)
     out = out or {}
     g = {}
     for n in ("dq_gen", "dk_gen", "dv_gen"):
-        g[n] = _out(out, n, (p.n_gen, H, d), torch.bfloat16, dev)
+        g[n] = _out(out, n, (n_gen, H, d), torch.bfloat16, dev)
     for n in ("dq_ref", "dk_ref", "dv_ref"):
-        g[n] = None if (go and n == "dq_ref") else \
-            _out(out, n, (p.n_ref, H, d), torch.bfloat16, dev)
-    nbytes = p.workspace_size(True)
-    ws = out.get("workspace")
-    if ws is None or ws.numel() < nbytes:
-        ws = _alloc_workspace(nbytes, dev)
+        g[n] = None if (go and n == "dq_ref") else _out(out, n, (n_ref, H, d), torch.bfloat16, dev)
+    ws = _workspace(out, p.workspace_size(True), dev)
     _check(lib().sra_backward(p.ptr, _ptr(q_gen), _ptr(k_gen), _ptr(v_gen), _ptr(q_ref), _ptr(k_ref),
                               _ptr(v_ref), _ptr(o_gen), _ptr(o_ref), _ptr(lse_gen), _ptr(lse_ref),
                               _ptr(do_gen), _ptr(do_ref), _ptr(g["dq_gen"]), _ptr(g["dk_gen"]),

@@ -16,7 +16,7 @@ def test_library_exports_every_declared_function():
     assert set(names) >= {"sra_workspace_size", "sra_forward", "sra_backward", "sra_pair_counts",
                           "sra_schedule_info", "sra_schedule_mask", "sra_schedule_export",
                           "sra_release_caches", "sra_status_string", "sra_last_error", "sra_version",
-                          "sra_kernel_timing_enable", "sra_kernel_timing"}
+                          "sra_kernel_timing_enable", "sra_kernel_timing", "sra_dense_mask"}
     L = sra.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -45,6 +45,10 @@ GOOD = [SampleGeom(2, 8, 8, 4, 8, 8)]
     # the largest accepted: heads * rows = 2^31 - 1 exactly (gen), and just below (ref)
     ([SampleGeom(1, 2147483647, 1, 0, 1, 1)], 1, 64, 0, None),
     ([SampleGeom(1, 1, 1, 1, 53687091, 1)], 40, 128, 0, None),
+    # token strides whose offsets inside a tile (63 rows past its first) would overflow int32
+    (GOOD, 2, 64, 33554432, sra.SRA_ERR_UNSUPPORTED),
+    (GOOD, 2, 64, 1 << 40, sra.SRA_ERR_UNSUPPORTED),
+    (GOOD, 2, 64, 33554424, "ok"),                        # the largest accepted multiple of 8
 ])
 def test_invalid_problems_are_rejected(samples, heads, d, stride, status):
     p = sra.Problem(samples, heads, d, gen_token_stride=stride)
@@ -57,6 +61,9 @@ def test_invalid_problems_are_rejected(samples, heads, d, stride, status):
         assert (gp.value, rp.value) == (G * (G + R), R * F)
         return
     st = sra.lib().sra_workspace_size(p.ptr, 0, ctypes.byref(n))
+    if status == "ok":
+        assert st == sra.SRA_OK and n.value > 0
+        return
     assert st == status
     assert len(sra.lib().sra_last_error()) > 0
 
@@ -166,3 +173,76 @@ def test_compacted_plans_reserve_the_compacted_reference_tensors():
     assert split.workspace_size(False) >= plain.workspace_size(False) - 4096 + 4 * rows
     assert split.workspace_size(True) >= plain.workspace_size(True) - 4096 + 8 * rows
     assert whole.workspace_size(False) < plain.workspace_size(False) + 4 * rows
+
+
+# ---------------------------------------------------------------- binding argument checks (CPU)
+def _tensors(H=1, d=64, G=128, R=256, device="cpu"):
+    import torch
+
+    def t(n):
+        return torch.zeros((n, H, d), dtype=torch.bfloat16, device=device)
+    return [t(G), t(G), t(G), t(R), t(R), t(R)]
+
+
+def _rejects(fn, *args, match=None, **kw):
+    with pytest.raises(sra.SRAError) as e:
+        fn(*args, **kw)
+    assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+    if match:
+        assert match in str(e.value), str(e.value)
+
+
+def test_binding_rejects_bad_inputs_before_the_library():
+    """dtype, shape and layout of q/k/v are checked against the geometry, then the device: a CPU
+    tensor never reaches the library (a device pointer of the wrong kind would fault the GPU)."""
+    import torch
+
+    qg, kg, vg, qr, kr, vr = _tensors()
+    _rejects(sra.forward, qg.float(), kg, vg, qr, kr, vr, GOOD, match="dtype")
+    _rejects(sra.forward, qg, kg[:100], vg, qr, kr, vr, GOOD, match="shape")
+    _rejects(sra.forward, qg, kg, vg, qr, kr[:, :, :32], vr, GOOD, match="shape")
+    q2, k2, v2, qr2, kr2, vr2 = _tensors(H=2)
+    _rejects(sra.forward, q2, k2, v2, qr2, kr2, vr2.transpose(1, 2).contiguous().transpose(1, 2), GOOD,
+             match="contiguous heads")
+    _rejects(sra.forward, qg, kg, vg, None, kr, vr, GOOD, match="q_ref")
+    _rejects(sra.forward, qg, kg, vg, qr, kr, vr, GOOD, match="GPU")
+    _rejects(sra.forward, qg.unsqueeze(0), kg, vg, qr, kr, vr, GOOD, match="q_gen")
+    # a tensor on another device than q_gen (the meta device stands in for a second GPU)
+    meta = torch.zeros((256, 1, 64), dtype=torch.bfloat16, device="meta")
+    with pytest.raises(sra.SRAError):
+        sra.forward(qg, kg, vg, qr, meta, vr, GOOD)
+
+
+def test_binding_rejects_bad_output_buffers():
+    import torch
+
+    qg, kg, vg, qr, kr, vr = _tensors()
+    bad = {
+        "o_gen": torch.zeros((128, 1, 64), dtype=torch.float32),
+        "lse_gen": torch.zeros((128, 1), dtype=torch.float32),
+        "o_ref": torch.zeros((256, 1, 128), dtype=torch.bfloat16)[:, :, :64],  # not dense
+        "lse_ref": torch.zeros((1, 256), dtype=torch.bfloat16),
+    }
+    for name, t in bad.items():
+        with pytest.raises(sra.SRAError) as e:
+            sra._forward_args(qg, kg, vg, qr, kr, vr, GOOD, None, {name: t}, False, None, None)
+        assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT and name in str(e.value)
+    with pytest.raises(sra.SRAError):
+        sra._workspace({"workspace": torch.zeros(16, dtype=torch.float32)}, 16, torch.device("cpu"))
+
+
+def test_binding_backward_checks_every_tensor():
+    import torch
+
+    qg, kg, vg, qr, kr, vr = _tensors()
+    og, org, dog, dor = qg, qr, qg, qr
+    lg, lr = torch.zeros((1, 128)), torch.zeros((1, 256))
+    args = [qg, kg, vg, qr, kr, vr, og, org, lg, lr, dog, dor]
+    cases = {6: og.float(), 8: lg.t(), 9: torch.zeros((1, 255)), 10: dog[:, :, :32],
+             11: qr.transpose(0, 1).contiguous().transpose(0, 1)}
+    for i, t in cases.items():
+        a = list(args)
+        a[i] = t
+        _rejects(sra.backward, *a, GOOD)
+    _rejects(sra.backward, *args, GOOD, match="GPU")
+    _rejects(sra.backward, *args, GOOD, out={"dk_ref": torch.zeros((256, 1, 64))}, match="dk_ref")

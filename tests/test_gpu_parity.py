@@ -317,8 +317,22 @@ def test_error_paths_do_not_launch():
     assert e.value.status == sra.SRA_ERR_WORKSPACE_TOO_SMALL
     torch.cuda.synchronize()
     assert torch.all(o["o_gen"].float() == 7.0)
-    with pytest.raises(ValueError):
+    # the binding checks every tensor against the geometry before the library sees it
+    with pytest.raises(sra.SRAError) as e:
         sra.forward(y["q_gen"][:10], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], samples)
+    assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+    o_gen, o_ref, l_gen, l_ref = sra.forward(*[y[n] for n in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")],
+                                             samples)
+    dq = torch.full((64, 1, 128), 7.0, dtype=torch.bfloat16, device=dev)
+    for bad in ({"do_gen": y["do_gen"].float()}, {"lse_gen": l_gen[:, :32]}, {"do_ref": y["do_ref"].cpu()}):
+        args = {"do_gen": y["do_gen"], "do_ref": y["do_ref"], "lse_gen": l_gen}
+        args.update(bad)
+        with pytest.raises(sra.SRAError) as e:
+            sra.backward(y["q_gen"], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], o_gen, o_ref,
+                         args["lse_gen"], l_ref, args["do_gen"], args["do_ref"], samples, out={"dq_gen": dq})
+        assert e.value.status == sra.SRA_ERR_INVALID_ARGUMENT
+    torch.cuda.synchronize()
+    assert torch.all(dq.float() == 7.0)
 
 
 # ------------------------------------------------------------------- reference as context only

@@ -50,6 +50,17 @@ GEOMS = [
 
 
 @pytest.mark.parametrize("gi", range(len(GEOMS)))
+def test_dense_mask_is_the_oracle_mask(gi):
+    """sra_dense_mask (the rule written out by the library) equals the oracle's mask, bit-exact."""
+    samples = GEOMS[gi]
+    for b, g in enumerate(samples):
+        want = oracle.visibility_mask(g).astype(np.uint8)
+        assert np.array_equal(sra.dense_mask(samples, b), want), b
+    with pytest.raises(sra.SRAError):
+        sra.dense_mask(samples, len(samples))
+
+
+@pytest.mark.parametrize("gi", range(len(GEOMS)))
 @pytest.mark.parametrize("which", SCHEDS)
 def test_schedule_mask_is_the_visibility_mask(gi, which):
     samples = GEOMS[gi]
