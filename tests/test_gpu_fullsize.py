@@ -146,10 +146,23 @@ def _sample_keys(geom, rng, n_rand=6):
     return np.array(sorted(gen) + sorted(G + r for r in ref), dtype=np.int64)
 
 
-@pytest.mark.parametrize("name", ["varlen_tokens", "varlen_window"])
-def test_fullsize_dkv_sampled_keys(name):
+def _keys_720p(geom, rng):
+    """Keys of the 720p layer at tile and frame edges: gen key tiles are 256 keys, and reference
+    key tiles run across frame boundaries (3,600 keys per frame = 14 tiles + 16 keys), so keys
+    3,584..3,839 share one tile whose first 16 keys belong to frame 0 and the rest to frame 1."""
+    G, R, F = geom.n_gen, geom.n_ref, geom.ref_h * geom.ref_w
+    gen = {0, 1, 255, 256, 257, G // 2, G - 257, G - 256, G - 1} | set(rng.integers(0, G, 3).tolist())
+    ref = {0, 255, 256, 3583, 3584, F - 1, F, F + 1, F + 239, F + 240, R - F, R - 1}
+    return np.array(sorted(gen) + sorted(G + r for r in ref), dtype=np.int64)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name,h", [("varlen_tokens", 1), ("varlen_window", 1), ("720p", 0), ("720p", 39)])
+def test_fullsize_dkv_sampled_keys(name, h):
     """dK/dV of sampled keys against the oracle's sums over every query that sees each key (the
-    sample with the shortest reference, one head; about 10 s of oracle time per case)."""
+    sample with the shortest reference, one head). The oracle runs every query row that sees a
+    sampled key through its full masked softmax: about 10 s per varlen case and 40 s per 720p
+    head (75,600 gen rows x 151,200 keys, fp32, in blocks of 2,048 rows) on 16 host threads."""
     w = workload(name)
     x = _inputs(w, grads=True)
     ins = [x[k] for k in INS]
@@ -159,11 +172,13 @@ def test_fullsize_dkv_sampled_keys(name):
     go, ro = _offsets(w.samples)
     b = int(np.argmin([s.n_ref for s in w.samples]))
     geom = w.samples[b]
-    h = 1
-    keys = _sample_keys(geom, np.random.default_rng(9))
+    big = name == "720p"
+    keys = _keys_720p(geom, np.random.default_rng(9)) if big else _sample_keys(geom, np.random.default_rng(9))
     xh = _head_view(x, h)
     print(f"[fullsize] {name} dK/dV head {h} sample {b}: {len(keys)} keys", flush=True)
-    want_k, want_v = oracle.dkv_keys(xh, w.samples, b, 0, keys)
+    want_k, want_v = oracle.dkv_keys(xh, w.samples, b, 0, keys, dtype=np.float32 if big else np.float64,
+                                     block_rows=2048)
+    want_k, want_v = want_k.astype(np.float64), want_v.astype(np.float64)
     G = geom.n_gen
     got_k = _gpu_rows(g["dk_gen"][:, h], g["dk_ref"][:, h], go, ro, b, G, keys)
     got_v = _gpu_rows(g["dv_gen"][:, h], g["dv_ref"][:, h], go, ro, b, G, keys)
