@@ -47,7 +47,7 @@ def _args():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="720p", help="720p (default) or varlen")
     ap.add_argument("--sweep-reps", type=int, default=2, help="forward calls per sweep point (0 = skip)")
-    ap.add_argument("--cpu-rows", type=int, default=3072, help="gen rows in the CPU-oracle sample (0 = skip)")
+    ap.add_argument("--cpu-rows", type=int, default=4096, help="gen rows in the CPU-oracle sample (0 = skip)")
     ap.add_argument("--tiny-reps", type=int, default=200, help="calls per pass of the tiny workload (0 = skip)")
     ap.add_argument("--other-reps", type=int, default=2,
                     help="timed calls per pass of the 480p and varlen workloads (0 = skip)")
@@ -244,64 +244,149 @@ def _other_workloads(sra, torch, reps):
     return res
 
 
-def _cpu_baseline(x_gpu, w, gen_rows, torch):
-    """The oracle (unchanged, float64, numpy BLAS) on a bounded sample of head 0."""
+def _cpu_info():
+    """Host CPU model and the cores this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        usable = os.cpu_count() or 1
+    return model, os.cpu_count() or 1, usable
+
+
+def _cpu_baseline(x_gpu, w, gen_rows, torch, layer_pairs):
+    """The oracle as it stands, timed on the host cores on bounded samples of the workload.
+
+    Legs (float32 unless stated, head 0):
+      fwd   forward_rows of gen_rows gen + gen_rows ref query rows of the layer (each row's
+            full key set), and the same rows in float64 beside it;
+      dq    dq_rows of gen_rows / 2 gen + gen_rows / 2 ref rows of the layer (S, P, O for D,
+            dP and dQ of each row, 8 d FLOP per visible pair);
+      slice the oracle's full forward and backward (explicit mask over all rows) on a slice of
+            the layer with the same per-frame shape: its first generation latent frame and its
+            first reference latent frame, plus dkv_keys (the sampled dK/dV entry point) on 64
+            of its keys;
+      tiny  the full forward and backward of the tiny workload.
+    Seconds per layer are extrapolated from the rates, by visible pairs: the forward from the
+    fwd leg (rows of the real layer), the backward from the slice's full backward. value is the
+    step's useful FLOP (4 d forward + 10 d backward per pair) over those extrapolated seconds.
+    """
     import numpy as np
 
     import oracle
+    from sra_inputs import SampleGeom, make_inputs, to_numpy64, workload
 
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
-        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        blas_threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = max(blas_threads, torch.get_num_threads())
+    model, ncpu, usable = _cpu_info()
+    d = w.head_dim
     g = w.samples[0]
-    G = g.n_gen
-    xh = {k: x_gpu[k][:, 0:1].float().cpu() for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")}
-    xh = {k: v.numpy() for k, v in xh.items()}
+    G, R, F = g.n_gen, g.n_ref, g.ref_h * g.ref_w
+    names = ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref", "do_gen", "do_ref")
+    xh = {k: x_gpu[k][:, 0:1].float().cpu().numpy() for k in names if k in x_gpu}
     rng = np.random.default_rng(0)
     rows_g = np.sort(rng.choice(G, size=min(gen_rows, G), replace=False))
-    rows_r = G + np.sort(rng.choice(g.n_ref, size=min(gen_rows, g.n_ref), replace=False)) if g.n_ref else np.zeros(0, int)
+    rows_r = G + np.sort(rng.choice(R, size=min(gen_rows, R), replace=False)) if R else np.zeros(0, int)
     rows = np.concatenate([rows_g, rows_r])
-    t0 = time.perf_counter()
-    for b0 in range(0, rows.size, 128):
-        blk = rows[b0:b0 + 128]
-        oracle.forward_rows(xh, w.samples, 0, 0, blk)
-    dt = time.perf_counter() - t0
-    # visible pairs of the sampled rows (closed form per stream for this geometry)
-    F = g.ref_h * g.ref_w
-    n_pairs = rows_g.size * (G + g.n_ref) + rows_r.size * F * g.group_frames
-    flops = 4 * w.head_dim * n_pairs
-    out = {
-        "value": round(flops / dt / 1e12, 6),
+
+    def pairs_of(n_gen_rows, n_ref_rows):
+        return n_gen_rows * (G + R) + n_ref_rows * F * g.group_frames
+
+    def timed_rows(fn, rr, dtype):
+        t = time.perf_counter()
+        for b0 in range(0, rr.size, 128):
+            fn(xh, w.samples, 0, 0, rr[b0:b0 + 128], dtype=dtype)
+        return time.perf_counter() - t
+
+    legs = {}
+    # forward rows of the real layer, fp32 (the oracle's precision) and fp64
+    t32 = timed_rows(oracle.forward_rows, rows, np.float32)
+    p_f = pairs_of(rows_g.size, rows_r.size)
+    legs["fwd"] = {"rows": int(rows.size), "visible_pairs": int(p_f), "s": round(t32, 2),
+                   "tflops": round(4 * d * p_f / t32 / 1e12, 6), "dtype": "float32"}
+    half = rows_g.size // 2
+    sub64 = np.concatenate([rows_g[:half // 2], rows_r[:half // 2]])
+    t64 = timed_rows(oracle.forward_rows, sub64, np.float64)
+    p64 = pairs_of(half // 2, min(half // 2, rows_r.size))
+    legs["fwd_float64"] = {"rows": int(sub64.size), "visible_pairs": int(p64), "s": round(t64, 2),
+                           "tflops": round(4 * d * p64 / t64 / 1e12, 6), "dtype": "float64"}
+    # dQ rows of the real layer (fp32): 8 d FLOP executed per visible pair
+    subq = np.concatenate([rows_g[:half], rows_r[:half]])
+    tq = timed_rows(oracle.dq_rows, subq, np.float32)
+    pq = pairs_of(min(half, rows_g.size), min(half, rows_r.size))
+    legs["dq"] = {"rows": int(subq.size), "visible_pairs": int(pq), "s": round(tq, 2),
+                  "executed_tflops": round(8 * d * pq / tq / 1e12, 6), "dtype": "float32"}
+    # slice of the layer: one gen frame and one ref frame, full forward + backward and dkv_keys
+    sl = [SampleGeom(1, g.gen_h, g.gen_w, 1, g.ref_h, g.ref_w)]
+    Gs, Rs = sl[0].n_gen, sl[0].n_ref
+    xs = {k: v[:(Gs if k.endswith("gen") else Rs)].astype(np.float32) for k, v in xh.items()}
+    gp_s, rp_s = oracle.pair_counts(sl)
+    t = time.perf_counter()
+    oracle.sra_forward(xs, sl, dtype=np.float32)
+    tf_s = time.perf_counter() - t
+    t = time.perf_counter()
+    oracle.sra_backward(xs, sl, dtype=np.float32)
+    tb_s = time.perf_counter() - t  # includes the forward it recomputes
+    keys = np.sort(rng.choice(Gs + Rs, size=64, replace=False))
+    t = time.perf_counter()
+    oracle.dkv_keys(xs, sl, 0, 0, keys, dtype=np.float32)
+    tk_s = time.perf_counter() - t
+    ps = gp_s + rp_s
+    legs["slice"] = {"geometry": f"gen 1x{g.gen_h}x{g.gen_w}, ref 1x{g.ref_h}x{g.ref_w}, 1 head",
+                     "visible_pairs": int(ps), "fwd_s": round(tf_s, 2), "bwd_s": round(tb_s, 2),
+                     "fwd_tflops": round(4 * d * ps / tf_s / 1e12, 6),
+                     "bwd_tflops": round(10 * d * ps / tb_s / 1e12, 6),
+                     "dkv_keys_64_s": round(tk_s, 2), "dtype": "float32"}
+    # the tiny workload, full forward and backward (fp32)
+    tw = workload("tiny")
+    xt = {k: to_numpy64(v).astype(np.float32)
+          for k, v in make_inputs(tw.samples, tw.heads, tw.head_dim, tw.seed, tw.rms_norm_qk).items()}
+    gt, rt = oracle.pair_counts(tw.samples)
+    t = time.perf_counter()
+    for _ in range(10):
+        oracle.sra_forward(xt, tw.samples, dtype=np.float32)
+    tft = (time.perf_counter() - t) / 10
+    t = time.perf_counter()
+    for _ in range(10):
+        oracle.sra_backward(xt, tw.samples, dtype=np.float32)
+    tbt = (time.perf_counter() - t) / 10
+    pt = (gt + rt) * tw.heads
+    legs["tiny"] = {"fwd_ms": round(tft * 1e3, 3), "bwd_ms": round(tbt * 1e3, 3),
+                    "fwd_tflops": round(4 * tw.head_dim * pt / tft / 1e12, 6),
+                    "bwd_tflops": round(10 * tw.head_dim * pt / tbt / 1e12, 6), "dtype": "float32"}
+    # per-layer extrapolation (all heads and samples), by visible pairs
+    fwd_rate = 4 * d * p_f / t32
+    bwd_rate = 10 * d * ps / tb_s
+    s_fwd = 4 * d * layer_pairs / fwd_rate
+    s_bwd = 10 * d * layer_pairs / bwd_rate
+    work = t32 + t64 + tq + tf_s + tb_s + tk_s + 10 * (tft + tbt)
+    return {
+        "value": round(14 * d * layer_pairs / (s_fwd + s_bwd) / 1e12, 6),
         "unit": "TFLOP/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"forward (O, LSE) of {rows_g.size} gen + {rows_r.size} ref query rows of head 0 "
-                  f"({n_pairs} visible pairs, {dt:.1f} s, float64 numpy); forward only",
+        "sample": (f"oracle in float32 on head 0 of sample 0 of the {w.name} layer: forward rows ({rows.size} rows), dQ rows "
+                   f"({subq.size} rows), and the full forward + backward of a one-gen-frame, one-ref-frame slice; "
+                   f"step rate = useful FLOP over the seconds per layer extrapolated from them ({work:.1f} s of "
+                   f"CPU work in all)"),
+        "cpu_model": model, "nproc": ncpu, "usable_cores": usable,
+        "blas_threads": blas_threads, "torch_threads": torch.get_num_threads(),
+        "seconds_per_layer_extrapolated": {"fwd": round(s_fwd, 1), "bwd": round(s_bwd, 1),
+                                           "step": round(s_fwd + s_bwd, 1)},
+        "legs": legs,
     }
-    # the same oracle on one thread against all threads, on the first 128 sampled rows of
-    # each stream
-    try:
-        from threadpoolctl import threadpool_limits
-    except Exception:  # pragma: no cover
-        return out
-    sub = np.concatenate([rows_g[:128], rows_r[:128]])
-    p1 = rows_g[:128].size * (G + g.n_ref) + rows_r[:128].size * F * g.group_frames
-
-    def run():
-        t = time.perf_counter()
-        oracle.forward_rows(xh, w.samples, 0, 0, sub)
-        return time.perf_counter() - t
-
-    t_all = run()
-    with threadpool_limits(limits=1):
-        t_one = run()
-    out["one_thread"] = {"value": round(4 * w.head_dim * p1 / t_one / 1e12, 6), "unit": "TFLOP/s", "cores": 1,
-                         "all_threads_value": round(4 * w.head_dim * p1 / t_all / 1e12, 6),
-                         "sample": f"forward of the first {rows_g[:128].size} gen + {rows_r[:128].size} ref sampled "
-                                   f"rows of head 0 in one block ({p1} visible pairs, {t_one:.1f} s on one thread)"}
-    return out
 
 
 def _gen_only(sra, torch, ins, fo, w, H, d, reps, line):
@@ -399,7 +484,7 @@ def main():
     dev = torch.device("cuda:0")
     H, d = w.heads, w.head_dim
     print(f"[bench] inputs {w.name}", file=sys.stderr, flush=True)
-    x = make_inputs(w.samples, H, d, w.seed, w.rms_norm_qk, device=dev)
+    x = make_inputs(w.samples, H, d, w.seed, w.rms_norm_qk, device=dev)  # with dO
     ins = [x[k] for k in ("q_gen", "k_gen", "v_gen", "q_ref", "k_ref", "v_ref")]
     G, R = ins[0].shape[0], ins[3].shape[0]
     bf = dict(dtype=torch.bfloat16, device=dev)
@@ -473,7 +558,7 @@ def main():
         _gen_only(sra, torch, ins, fo, w, H, d, go_reps, line)
     if args.cpu_rows > 0:
         print("[bench] cpu oracle sample", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = _cpu_baseline(x, w, args.cpu_rows, torch)
+        line["cpu_baseline"] = _cpu_baseline(x, w, args.cpu_rows, torch, pairs)
     del x, ins, fo, bo
     torch.cuda.empty_cache()
     if args.sweep_reps > 0:

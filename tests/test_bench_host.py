@@ -73,3 +73,27 @@ def test_stored_traffic_is_dropped_when_the_kernel_source_changes(tmp_path, monk
     stored["kernels"]["dkdv"]["source_hash"] = "0" * 16
     p.write_text(json.dumps(stored))
     assert bench._stored_traffic("dkdv", "720p") is None
+
+
+def test_cpu_baseline_reports_fp32_legs_and_an_extrapolated_layer():
+    """The CPU-oracle leg of the benchmark on a small layer: float32 forward rows (float64
+    beside), dQ rows, the full forward and backward of a frame slice and the tiny workload,
+    seconds per layer extrapolated from them, and the host's CPU description."""
+    import torch
+
+    from paper_2606_13872_amd import sra
+    from sra_inputs import SampleGeom, Workload, make_inputs
+
+    w = Workload("small", [SampleGeom(3, 8, 8, 3, 8, 8)], 2, 64, 5, False)
+    x = make_inputs(w.samples, w.heads, w.head_dim, w.seed)
+    fwd, _ = sra.useful_flops(w.samples, w.heads, w.head_dim)
+    out = bench._cpu_baseline(x, w, 32, torch, fwd // (4 * w.head_dim))
+    assert out["kind"] == "oracle" and out["unit"] == "TFLOP/s" and out["value"] > 0
+    assert out["cores"] >= 1 and out["nproc"] >= 1 and isinstance(out["cpu_model"], str)
+    legs = out["legs"]
+    assert legs["fwd"]["dtype"] == "float32" and legs["fwd_float64"]["dtype"] == "float64"
+    assert legs["fwd"]["visible_pairs"] == 32 * (192 + 192) + 32 * 64
+    for k in ("dq", "slice", "tiny"):
+        assert k in legs
+    s = out["seconds_per_layer_extrapolated"]
+    assert s["step"] == pytest.approx(s["fwd"] + s["bwd"], abs=0.11)
