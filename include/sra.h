@@ -144,6 +144,35 @@ sra_status sra_backward(const sra_problem* p,
                         void* dq_ref, void* dk_ref, void* dv_ref,
                         void* workspace, size_t workspace_bytes, void* stream);
 
+/* ---- allocation-free forward ------------------------------------------------------------ */
+
+/* Size in bytes of the library's static device scratch array, the workspace of
+ * sra_forward_noalloc (one array per device, held from the first such call on that device until
+ * the process ends). */
+#define SRA_NOALLOC_WORKSPACE_MAX (32u << 20)
+
+/* For callers that cannot allocate device memory (code under stream capture, tight serving
+ * loops, harnesses that forbid hipMalloc): sra_forward with the workspace taken from the
+ * library's static scratch array on the current device instead of a caller buffer. Same
+ * kernels, so results are bitwise those of sra_forward.
+ * In/out tensors, stream and validation as sra_forward; `stream` must belong to the current
+ * device (else SRA_ERR_INVALID_ARGUMENT). A problem whose workspace (sra_workspace_size with
+ * backward = 0) exceeds SRA_NOALLOC_WORKSPACE_MAX is rejected with SRA_ERR_WORKSPACE_TOO_SMALL
+ * before anything is enqueued: in practice every problem whose token masks do not force the
+ * compacted reference stream fits (the 720p layer needs 0.8 MB).
+ * Allocates no device memory and no pinned host memory (no hipMalloc, hipHostMalloc or
+ * hipFree): the schedule tables are copied from the plan's host image, and not at all when the
+ * previous sra_forward_noalloc call on this device used the same geometry and stream (the
+ * array keeps the last call's tables). A geometry not seen before is planned in host heap
+ * memory, as for every entry point.
+ * All calls on one device share one array: calls that overlap on a device (different streams
+ * or threads without ordering between them) race and may read each other's tables. */
+sra_status sra_forward_noalloc(const sra_problem* p,
+                               const void* q_gen, const void* k_gen, const void* v_gen,
+                               const void* q_ref, const void* k_ref, const void* v_ref,
+                               void* o_gen, void* o_ref, float* lse_gen, float* lse_ref,
+                               void* stream);
+
 /* ---- host-only inspection hooks (no device needed; used to test the schedules) ---------- */
 
 /* Visible (query, key) pairs per head summed over samples: the work of the attention, which

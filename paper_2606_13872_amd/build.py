@@ -19,7 +19,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsra.so")
 
 SOURCES = ["schedule.cpp", "sra_api.cpp", "sra_fwd.hip", "sra_bwd.hip", "sra_dq.hip", "sra_dkv.hip",
-           "sra_compact.hip"]
+           "sra_compact.hip", "sra_noalloc.hip"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", "-Wall",

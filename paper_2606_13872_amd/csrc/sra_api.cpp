@@ -13,6 +13,7 @@
 #include "sra.h"
 #include "schedule.hpp"
 #include "sra_kernels.h"
+#include "sra_internal.h"
 
 namespace {
 
@@ -216,6 +217,44 @@ PlanCache& cache() {
   return *c;
 }
 
+// Schedules resident in the static scratch of each device (the allocation-free forward). The
+// scratch keeps the last call's tables, so a call with the plan and stream of the previous
+// call on that device skips the upload; any other call copies the tables from the plan's host
+// image (pageable memory, so no pinned staging is allocated).
+class ResidentTables {
+ public:
+  sra_status upload(const Blob& b, uint64_t plan_id, int device, void* dst, hipStream_t s) {
+    std::lock_guard<std::mutex> lk(mu_);
+    Entry& e = by_device_[device];
+    if (e.plan_id == plan_id && e.stream == s) return SRA_OK;
+    e.plan_id = 0;
+    if (!b.image.empty()) {
+      hipError_t r = hipMemcpyAsync(dst, b.image.data(), b.image.size(), hipMemcpyHostToDevice, s);
+      if (r != hipSuccess) return fail(SRA_ERR_HIP, std::string("schedule upload: ") + hipGetErrorString(r));
+    }
+    e.plan_id = plan_id;
+    e.stream = s;
+    return SRA_OK;
+  }
+  void clear() {
+    std::lock_guard<std::mutex> lk(mu_);
+    by_device_.clear();
+  }
+
+ private:
+  struct Entry {
+    uint64_t plan_id = 0;
+    hipStream_t stream = nullptr;
+  };
+  std::mutex mu_;
+  std::unordered_map<int, Entry> by_device_;
+};
+
+ResidentTables& resident() {
+  static ResidentTables* r = new ResidentTables();
+  return *r;
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 // Bytes of `rows` dense bf16 rows of all heads, and of one fp32 value per (head, row).
@@ -360,10 +399,14 @@ sra_status sra_workspace_size(const sra_problem* p, int backward, size_t* bytes)
   return SRA_OK;
 }
 
-sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
-                       const void* q_ref, const void* k_ref, const void* v_ref, void* o_gen, void* o_ref,
-                       float* lse_gen, float* lse_ref, void* workspace, size_t workspace_bytes,
-                       void* stream) {
+}  // extern "C"
+
+namespace sra {
+
+sra_status forward_call(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
+                        const void* q_ref, const void* k_ref, const void* v_ref, void* o_gen, void* o_ref,
+                        float* lse_gen, float* lse_ref, void* workspace, size_t workspace_bytes, void* stream,
+                        const StaticWorkspace* sw) {
   g_last_error.clear();
   Layout L;
   std::shared_ptr<CachedPlan> cp;
@@ -373,6 +416,15 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
                   : check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen}, {q_ref, k_ref, v_ref, o_ref, lse_ref});
   if (st != SRA_OK) return st;
   const size_t need = fwd_workspace(*cp);
+  if (sw) {
+    if (need > sw->bytes)
+      return fail(SRA_ERR_WORKSPACE_TOO_SMALL, "forward needs " + std::to_string(need) +
+                                                   " workspace bytes, more than the static scratch maximum of " +
+                                                   std::to_string(sw->bytes));
+    if (!sw->ptr) return fail(SRA_ERR_INTERNAL, "static scratch has no device address");
+    workspace = sw->ptr;
+    workspace_bytes = sw->bytes;
+  }
   if (workspace_bytes < need)
     return fail(SRA_ERR_WORKSPACE_TOO_SMALL, "forward needs " + std::to_string(need) + " workspace bytes");
   if (need && (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign)))
@@ -380,7 +432,8 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
-  st = cache().upload(cp->fwd, ws, s);
+  if (sw) st = resident().upload(cp->fwd, cp->id, sw->device, ws, s);
+  else st = cache().upload(cp->fwd, ws, s);
   if (st != SRA_OK) return st;
   const Plan& P = cp->plan;
   const Layout& E = P.exec;
@@ -464,6 +517,20 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
     if (e != hipSuccess) return hip_fail(e, "fill launch");
   }
   return SRA_OK;
+}
+
+sra_status set_error(sra_status s, const char* msg) { return fail(s, msg); }
+
+}  // namespace sra
+
+extern "C" {
+
+sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
+                       const void* q_ref, const void* k_ref, const void* v_ref, void* o_gen, void* o_ref,
+                       float* lse_gen, float* lse_ref, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  return sra::forward_call(p, q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, lse_ref,
+                           workspace, workspace_bytes, stream, nullptr);
 }
 
 sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
@@ -769,6 +836,7 @@ sra_status sra_kernel_timing(int kernel, double* total_ms, int64_t* launches) {
 sra_status sra_release_caches(void) {
   g_last_error.clear();
   cache().clear();
+  resident().clear();
   return SRA_OK;
 }
 

@@ -1,0 +1,28 @@
+// Library-internal entry points shared by the C ABI translation units.
+#pragma once
+#include <stddef.h>
+
+#include "sra.h"
+
+namespace sra {
+
+// The device workspace of the allocation-free forward: the library's static scratch array on
+// the current device (its address as hipGetSymbolAddress gave it) and its size.
+struct StaticWorkspace {
+  void* ptr;
+  size_t bytes;
+  int device;
+};
+
+// sra_forward, with the workspace taken from `sw` when it is not null (the caller's workspace
+// arguments are then ignored, problems needing more than sw->bytes are rejected, and the
+// schedule is copied from pageable host memory only when it is not already resident).
+sra_status forward_call(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
+                        const void* q_ref, const void* k_ref, const void* v_ref, void* o_gen, void* o_ref,
+                        float* lse_gen, float* lse_ref, void* workspace, size_t workspace_bytes, void* stream,
+                        const StaticWorkspace* sw);
+
+// Sets the thread's last-error message and returns `s`.
+sra_status set_error(sra_status s, const char* msg);
+
+}  // namespace sra

@@ -75,6 +75,7 @@ def lib() -> ctypes.CDLL:
     sig = {
         "sra_workspace_size": [P, ctypes.c_int, ctypes.POINTER(sz)],
         "sra_forward": [P] + [vp] * 6 + [vp, vp, vp, vp] + [vp, sz, vp],
+        "sra_forward_noalloc": [P] + [vp] * 6 + [vp, vp, vp, vp] + [vp],
         "sra_backward": [P] + [vp] * 6 + [vp, vp, vp, vp, vp, vp] + [vp] * 6 + [vp, sz, vp],
         "sra_pair_counts": [P, ctypes.POINTER(i64), ctypes.POINTER(i64)],
         "sra_schedule_info": [P, ctypes.c_int, ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)],
@@ -86,6 +87,8 @@ def lib() -> ctypes.CDLL:
         "sra_kernel_timing": [ctypes.c_int, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)],
     }
     for name, args in sig.items():
+        if not hasattr(L, name):  # the host-only build has no sra_forward_noalloc (device code)
+            continue
         fn = getattr(L, name)
         fn.argtypes = args
         fn.restype = ctypes.c_int
@@ -460,6 +463,26 @@ def forward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[f
                              _ptr(v_ref), _ptr(o_gen), _ptr(o_ref), _ptr(lse_gen), _ptr(lse_ref),
                              _ptr(ws), ctypes.c_size_t(ws.numel()), _stream_ptr(dev)))
     return o_gen, o_ref, lse_gen, lse_ref
+
+
+def forward_noalloc(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale: Optional[float] = None,
+                    out: Optional[Dict] = None, gen_queries_only: bool = False):
+    """sra_forward_noalloc: the forward with the library's static device scratch as its
+    workspace. With every output in `out` the call allocates nothing on the device (no torch
+    allocation either). Same arguments and results as forward (a workspace in `out` is
+    ignored); problems whose workspace exceeds noalloc_workspace_max() raise SRAError."""
+    p, q_ref, o_gen, o_ref, lse_gen, lse_ref, out, dev = _forward_args(
+        q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, scale, out, gen_queries_only, None, None)
+    _check(lib().sra_forward_noalloc(p.ptr, _ptr(q_gen), _ptr(k_gen), _ptr(v_gen), _ptr(q_ref), _ptr(k_ref),
+                                     _ptr(v_ref), _ptr(o_gen), _ptr(o_ref), _ptr(lse_gen), _ptr(lse_ref),
+                                     _stream_ptr(dev)))
+    return o_gen, o_ref, lse_gen, lse_ref
+
+
+def noalloc_workspace_max() -> int:
+    """SRA_NOALLOC_WORKSPACE_MAX of include/sra.h (bytes)."""
+    m = re.search(r"#define\s+SRA_NOALLOC_WORKSPACE_MAX\s+\((\d+)u\s*<<\s*(\d+)\)", open(HEADER_PATH).read())
+    return int(m.group(1)) << int(m.group(2))
 
 
 def backward(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, lse_ref, do_gen, do_ref,

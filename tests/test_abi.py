@@ -4,6 +4,7 @@ No device work happens here: every call either fails validation before anything 
 enqueued or is a host-only hook.
 """
 import ctypes
+import os
 
 import pytest
 
@@ -11,6 +12,10 @@ from paper_2606_13872_amd import sra
 from sra_inputs import SampleGeom
 
 
+HOST_ONLY = bool(os.environ.get("SRA_HOST_LIB"))  # the sanitizer run's host-only library
+
+
+@pytest.mark.skipif(HOST_ONLY, reason="the host-only sanitizer build has no device entry points")
 def test_library_exports_every_declared_function():
     names = sra.header_functions()
     assert set(names) >= {"sra_workspace_size", "sra_forward", "sra_backward", "sra_pair_counts",
@@ -246,3 +251,20 @@ def test_binding_backward_checks_every_tensor():
         _rejects(sra.backward, *a, GOOD)
     _rejects(sra.backward, *args, GOOD, match="GPU")
     _rejects(sra.backward, *args, GOOD, out={"dk_ref": torch.zeros((256, 1, 64))}, match="dk_ref")
+
+
+@pytest.mark.skipif(HOST_ONLY, reason="the host-only sanitizer build has no device entry points")
+def test_noalloc_forward_rejects_oversized_problems_on_the_host():
+    """The allocation-free forward takes its workspace from a static array of
+    SRA_NOALLOC_WORKSPACE_MAX bytes; a problem needing more (here a token mask that forces the
+    compacted reference stream at 40 heads) is rejected before any device call."""
+    tok = [1, 0] * 1024 + [1] * 2048
+    p = sra.Problem([SampleGeom(1, 4, 4, 2, 32, 64, ref_token_valid=tok)], 40, 128)
+    assert p.workspace_size(False) > sra.noalloc_workspace_max() == 32 << 20
+    fake = ctypes.c_void_p(1 << 20)
+    st = sra.lib().sra_forward_noalloc(p.ptr, *([fake] * 10), ctypes.c_void_p(0))
+    assert st == sra.SRA_ERR_WORKSPACE_TOO_SMALL
+    assert b"static scratch maximum" in sra.lib().sra_last_error()
+    # validation errors come first, as for sra_forward
+    bad = sra.Problem([SampleGeom(0, 4, 4, 2, 4, 4)], 1, 64)
+    assert sra.lib().sra_forward_noalloc(bad.ptr, *([fake] * 10), ctypes.c_void_p(0)) == sra.SRA_ERR_INVALID_ARGUMENT
