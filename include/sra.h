@@ -166,7 +166,8 @@ sra_status sra_backward(const sra_problem* p,
  * array keeps the last call's tables). A geometry not seen before is planned in host heap
  * memory, as for every entry point.
  * All calls on one device share one array: calls that overlap on a device (different streams
- * or threads without ordering between them) race and may read each other's tables. */
+ * or threads without ordering between them) race and may read each other's tables. The first
+ * call on a device loads the array there (a one-time cost of milliseconds). */
 sra_status sra_forward_noalloc(const sra_problem* p,
                                const void* q_gen, const void* k_gen, const void* v_gen,
                                const void* q_ref, const void* k_ref, const void* v_ref,

@@ -406,7 +406,7 @@ namespace sra {
 sra_status forward_call(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,
                         const void* q_ref, const void* k_ref, const void* v_ref, void* o_gen, void* o_ref,
                         float* lse_gen, float* lse_ref, void* workspace, size_t workspace_bytes, void* stream,
-                        const StaticWorkspace* sw) {
+                        StaticWorkspaceFn static_ws, size_t static_bytes) {
   g_last_error.clear();
   Layout L;
   std::shared_ptr<CachedPlan> cp;
@@ -416,14 +416,19 @@ sra_status forward_call(const sra_problem* p, const void* q_gen, const void* k_g
                   : check_tensors(L, {q_gen, k_gen, v_gen, o_gen, lse_gen}, {q_ref, k_ref, v_ref, o_ref, lse_ref});
   if (st != SRA_OK) return st;
   const size_t need = fwd_workspace(*cp);
-  if (sw) {
-    if (need > sw->bytes)
+  StaticWorkspace sws{nullptr, 0, -1};
+  const StaticWorkspace* sw = nullptr;
+  if (static_ws) {
+    if (need > static_bytes)
       return fail(SRA_ERR_WORKSPACE_TOO_SMALL, "forward needs " + std::to_string(need) +
                                                    " workspace bytes, more than the static scratch maximum of " +
-                                                   std::to_string(sw->bytes));
-    if (!sw->ptr) return fail(SRA_ERR_INTERNAL, "static scratch has no device address");
-    workspace = sw->ptr;
-    workspace_bytes = sw->bytes;
+                                                   std::to_string(static_bytes) + " (use sra_forward)");
+    st = static_ws(stream, &sws);
+    if (st != SRA_OK) return st;
+    if (!sws.ptr) return fail(SRA_ERR_INTERNAL, "static scratch has no device address");
+    sw = &sws;
+    workspace = sws.ptr;
+    workspace_bytes = sws.bytes;
   }
   if (workspace_bytes < need)
     return fail(SRA_ERR_WORKSPACE_TOO_SMALL, "forward needs " + std::to_string(need) + " workspace bytes");
@@ -530,7 +535,7 @@ sra_status sra_forward(const sra_problem* p, const void* q_gen, const void* k_ge
                        float* lse_gen, float* lse_ref, void* workspace, size_t workspace_bytes,
                        void* stream) {
   return sra::forward_call(p, q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, lse_ref,
-                           workspace, workspace_bytes, stream, nullptr);
+                           workspace, workspace_bytes, stream, nullptr, 0);
 }
 
 sra_status sra_backward(const sra_problem* p, const void* q_gen, const void* k_gen, const void* v_gen,

@@ -36,22 +36,9 @@ sra_status scratch_address(int device, void** out) {
   return SRA_OK;
 }
 
-}  // namespace
-
-extern "C" sra_status sra_forward_noalloc(const sra_problem* p, const void* q_gen, const void* k_gen,
-                                          const void* v_gen, const void* q_ref, const void* k_ref,
-                                          const void* v_ref, void* o_gen, void* o_ref, float* lse_gen,
-                                          float* lse_ref, void* stream) {
-  // the size check runs on the host before any device call
-  size_t need = 0;
-  sra_status st = sra_workspace_size(p, 0, &need);
-  if (st != SRA_OK) return st;
-  if (need > SRA_NOALLOC_WORKSPACE_MAX) {
-    const std::string msg = "forward needs " + std::to_string(need) +
-                            " workspace bytes, more than the static scratch maximum of " +
-                            std::to_string(size_t(SRA_NOALLOC_WORKSPACE_MAX)) + " (use sra_forward)";
-    return sra::set_error(SRA_ERR_WORKSPACE_TOO_SMALL, msg.c_str());
-  }
+// The static workspace of the stream's device: the current device, which the stream must belong
+// to (the scratch address is per device).
+sra_status static_workspace(void* stream, sra::StaticWorkspace* sw) {
   int device = -1;
   const hipError_t e = hipGetDevice(&device);
   if (e != hipSuccess) {
@@ -59,7 +46,7 @@ extern "C" sra_status sra_forward_noalloc(const sra_problem* p, const void* q_ge
     return sra::set_error(SRA_ERR_HIP, msg.c_str());
   }
   if (device < 0 || device >= kMaxDevices) return sra::set_error(SRA_ERR_UNSUPPORTED, "device index beyond 63");
-  if (stream) {  // the scratch address is per device: the stream must be the current device's
+  if (stream) {
     int sdev = -1;
     const hipError_t es = hipStreamGetDevice(static_cast<hipStream_t>(stream), &sdev);
     if (es != hipSuccess) {
@@ -72,9 +59,18 @@ extern "C" sra_status sra_forward_noalloc(const sra_problem* p, const void* q_ge
       return sra::set_error(SRA_ERR_INVALID_ARGUMENT, msg.c_str());
     }
   }
-  sra::StaticWorkspace sw{nullptr, size_t(SRA_NOALLOC_WORKSPACE_MAX), device};
-  st = scratch_address(device, &sw.ptr);
-  if (st != SRA_OK) return st;
+  sw->bytes = SRA_NOALLOC_WORKSPACE_MAX;
+  sw->device = device;
+  return scratch_address(device, &sw->ptr);
+}
+
+}  // namespace
+
+extern "C" sra_status sra_forward_noalloc(const sra_problem* p, const void* q_gen, const void* k_gen,
+                                          const void* v_gen, const void* q_ref, const void* k_ref,
+                                          const void* v_ref, void* o_gen, void* o_ref, float* lse_gen,
+                                          float* lse_ref, void* stream) {
+  // validation and the size check run on the host before any device call
   return sra::forward_call(p, q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, o_gen, o_ref, lse_gen, lse_ref,
-                           nullptr, 0, stream, &sw);
+                           nullptr, 0, stream, static_workspace, SRA_NOALLOC_WORKSPACE_MAX);
 }

@@ -101,6 +101,12 @@ def box_token_mask(ref_frames: int, ref_h: int, ref_w: int, seed: int, p_frame_i
 
 
 def workload(name: str) -> Workload:
+    """The named workload; "<name>@h<N>" is that workload with N heads (a GPU's share of the
+    heads when the layer is split across GPUs by head), same geometry and seed."""
+    if "@h" in name:
+        base, heads = name.split("@h", 1)
+        w = workload(base)
+        return Workload(name, w.samples, int(heads), w.head_dim, w.seed, w.rms_norm_qk)
     if name == "tiny":
         return Workload(name, [SampleGeom(2, 8, 8, 4, 8, 8)], 1, 64, 0, False)
     if name == "480p":
