@@ -122,15 +122,23 @@ sra_status make_layout(const sra_problem* p, Layout* out, std::string* err) {
     int64_t open = -1;  // first row of the run being extended, -1 = none
     for (int32_t f = 0; f < g.ref_frames; ++f) {
       const bool fv = !g.ref_frame_valid || g.ref_frame_valid[f];
+      if (!g.ref_token_valid) {  // a frame mask alone: whole frames open or close a run
+        const int64_t r = int64_t(f) * s.F;
+        if (fv && open < 0) open = r;
+        if (!fv && open >= 0) {
+          s.vruns.push_back({open, r});
+          open = -1;
+        }
+        continue;
+      }
       for (int64_t j = 0; j < s.F; ++j) {
         const int64_t r = int64_t(f) * s.F + j;
-        const bool tv = fv && (!g.ref_token_valid || g.ref_token_valid[r]);
+        const bool tv = fv && g.ref_token_valid[r];
         if (tv && open < 0) open = r;
         if (!tv && open >= 0) {
           s.vruns.push_back({open, r});
           open = -1;
         }
-        if (!g.ref_token_valid && !fv) break;  // a frame mask alone: skip the frame's rows
       }
     }
     if (open >= 0) s.vruns.push_back({open, s.R});

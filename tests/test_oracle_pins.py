@@ -432,6 +432,23 @@ def test_key_block_mode_matches_full():
                 np.testing.assert_allclose(dk[i], want_k, rtol=1e-10, atol=1e-13)
                 np.testing.assert_allclose(dv[i], want_v, rtol=1e-10, atol=1e-13)
 
+def test_mask_blocks_of_rows_and_columns_are_the_full_mask():
+    """The mask built for a block of rows and a selection of key columns (the block mode that
+    dkv_keys uses to find the query rows seeing its keys) is that block of the full mask, for
+    contiguous and scattered selections, with windows, groups and token masks."""
+    rng = np.random.default_rng(5)
+    tok = (rng.random(4 * 12) < 0.6).astype(np.uint8).tolist()
+    for geom in (SampleGeom(3, 4, 5, 4, 3, 4, group_frames=2, frame_valid=[1, 0, 1, 1], ref_token_valid=tok),
+                 SampleGeom(5, 2, 3, 2, 3, 3, gen_window=1), SampleGeom(2, 3, 3, 0, 1, 1)):
+        full = oracle.visibility_mask(geom)
+        n = full.shape[0]
+        for rows, cols in ((np.arange(n), np.arange(n)), (np.arange(3, n - 2), np.arange(1, n)),
+                           (np.sort(rng.choice(n, 7, replace=False)), np.sort(rng.choice(n, 9, replace=False))),
+                           (np.arange(n), np.array([0, n - 1])), (np.array([n - 1]), np.arange(n))):
+            np.testing.assert_array_equal(oracle.visibility_mask(geom, rows, cols), full[np.ix_(rows, cols)])
+        np.testing.assert_array_equal(oracle.visibility_mask(geom, np.arange(n)), full)
+
+
 def test_varlen_samples_do_not_interact():
     samples = [SampleGeom(1, 2, 4, 2, 2, 4), SampleGeom(2, 2, 2, 1, 2, 4)]
     x = rand_inputs(samples, 1, 8, grads=True)
