@@ -426,3 +426,33 @@ def test_caller_buffers_are_filled_in_place():
         assert torch.equal(t, u)
     for n in ga:
         assert torch.equal(ga[n], gb[n]), n
+
+
+def test_plan_cache_eviction_and_staging_reuse():
+    """More geometries than the plan cache holds (256): plans are evicted while their uploads
+    may still be in flight, and later plans reuse their pinned staging buffers. Every call is
+    checked by the K = 0 count law (LSE = ln |visible keys|), and the first geometries, run again
+    after their plans were evicted (and after sra_release_caches), give bitwise the same results."""
+    dev = torch.device("cuda")
+    geoms = [[SampleGeom(1 + i % 3, 2 + i % 5, 3 + (i // 5) % 7, 1 + (i // 35) % 3, 2 + i % 4, 3)] for i in range(300)]
+    assert len({tuple(g) for g in geoms}) == 300
+    first = {}
+    for rep in range(3):  # all of them; the first 12 again (evicted); again after release_caches
+        for i, samples in enumerate(geoms if rep == 0 else geoms[:12]):
+            x = make_inputs(samples, 1, 64, 100 + i)
+            y = {k: v.to(dev) for k, v in x.items()}
+            y["k_gen"].zero_()
+            y["k_ref"].zero_()
+            o = sra.forward(y["q_gen"], y["k_gen"], y["v_gen"], y["q_ref"], y["k_ref"], y["v_ref"], samples)
+            g = samples[0]
+            lg = o[2].double().cpu().numpy()
+            assert np.allclose(lg, math.log(g.n_gen + g.n_ref), atol=1e-5), i
+            lr = o[3].double().cpu().numpy()
+            assert np.allclose(lr, math.log(g.ref_h * g.ref_w), atol=1e-5), i
+            if rep == 0 and i < 12:
+                first[i] = [t.clone() for t in o]
+            elif rep > 0:
+                for a, b in zip(first[i], o):
+                    assert torch.equal(a, b), (rep, i)
+        if rep == 1:
+            sra.release_caches()
