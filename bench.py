@@ -36,7 +36,9 @@ KERNEL_SYMBOLS = {"forward": "sra_fwd_kernel", "dkdv": "sra_dkv_kernel", "dq": "
                   "delta": "sra_delta_kernel"}
 KERNEL_SOURCES = {"forward": ["sra_fwd.hip"], "dkdv": ["sra_dkv.hip"], "dq": ["sra_dq.hip"],
                   "delta": ["sra_bwd.hip"]}
-COMMON_SOURCES = ["sra_config.h", "sra_device.h", "sra_tiles.h", "sra_kernels.h"]
+# schedule.cpp sets the launch order of the work items, which decides how often a tile is
+# fetched again from HBM
+COMMON_SOURCES = ["sra_config.h", "sra_device.h", "sra_tiles.h", "sra_kernels.h", "schedule.cpp"]
 COPY_KERNEL = "neg_kernel"  # calibration: torch.neg over a float32 buffer reads and writes it once
 
 

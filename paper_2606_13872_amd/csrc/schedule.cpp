@@ -221,10 +221,17 @@ void emit_items(const TileClass& c, int tile, int32_t heads, int step,
 
 // Orders items for launch. Workgroups are dealt round-robin over the 8 XCDs, so item k of
 // the launch order runs on XCD k % 8 and each XCD consumes its own subsequence in order.
-// When heads divide evenly over the XCDs, every head is pinned to one XCD (its K/V stay in
-// that XCD's L2) and each XCD's subsequence is longest-first; otherwise the whole list is
-// longest-first and the round-robin deal balances it.
-void order_items(std::vector<std::pair<int64_t, WorkItem>>& v, int32_t heads, Schedule* s) {
+// When heads divide evenly over the XCDs, every head is pinned to one XCD (the rows it streams
+// stay in that XCD's L2) and each XCD's subsequence is longest-first; otherwise the whole list
+// is longest-first and the round-robin deal balances it.
+// heads_in_turn: each XCD runs its heads one after another instead, each head's items
+// longest-first. For key tiles, whose items are of a few similar lengths and all stream the
+// head's gen queries from the first row, this keeps the workgroups resident on an XCD on one
+// head and close together in its query stream (measured at 720p: half the L2 misses, 1.5 %
+// faster). Query tiles keep the plain order: there the long gen tiles of all the XCD's heads
+// run back to back in step, and putting each head's short ref tiles between them staggered
+// the next head's start and nearly tripled the misses.
+void order_items(std::vector<std::pair<int64_t, WorkItem>>& v, int32_t heads, bool heads_in_turn, Schedule* s) {
   std::stable_sort(v.begin(), v.end(), [](const auto& a, const auto& b) { return a.first > b.first; });
   s->real_items = int64_t(v.size());
   s->items.clear();
@@ -234,6 +241,9 @@ void order_items(std::vector<std::pair<int64_t, WorkItem>>& v, int32_t heads, Sc
   }
   std::vector<std::vector<WorkItem>> per(kNumXcd);
   for (auto& e : v) per[e.second.head % kNumXcd].push_back(e.second);
+  if (heads_in_turn)
+    for (auto& q : per)
+      std::stable_sort(q.begin(), q.end(), [](const WorkItem& a, const WorkItem& b) { return a.head < b.head; });
   size_t n = 0;
   for (auto& q : per) n = std::max(n, q.size());
   WorkItem pad{};
@@ -282,7 +292,7 @@ void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
   }
   std::vector<std::pair<int64_t, WorkItem>> v;
   for (const TileClass& c : classes) emit_items(c, tile, L.heads, step, s->spans, &v);
-  order_items(v, L.heads, s);
+  order_items(v, L.heads, false, s);
 }
 
 // First frame of the ref group holding sample-relative ref row r.
@@ -365,7 +375,7 @@ void build_key_major(const Layout& L, int tile, int step, Schedule* s) {
     }
   }
   for (const TileClass& c : classes) emit_items(c, tile, L.heads, step, s->spans, &v);
-  order_items(v, L.heads, s);
+  order_items(v, L.heads, true, s);
 }
 
 }  // namespace

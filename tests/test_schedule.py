@@ -152,16 +152,26 @@ def test_schedule_tables_are_well_formed(which):
             assert cov.max() <= 1
 
 
-def test_xcd_order_pins_heads_and_puts_long_items_first():
+@pytest.mark.parametrize("which", [0, 1, 2])
+def test_xcd_order_pins_heads_and_puts_long_items_first(which):
+    """Each XCD's subsequence (items k, k + 8, ...) holds the heads pinned to it. Query tiles
+    (forward, dQ) run longest-first over the XCD's heads; key tiles (dK/dV) run the heads one
+    after another, each head's items longest-first."""
     w = workload("480p")
-    items, spans = sra.schedule_export(w.samples, sra.SCHED_FORWARD, w.heads, w.head_dim)
+    items, spans = sra.schedule_export(w.samples, which, w.heads, w.head_dim)
     assert len(items) % 8 == 0
+    key_major = which == sra.SCHED_BWD_DKDV
     for x in range(8):
         sub = items[x::8]
         sub = sub[sub[:, 0] >= 0]
         assert np.all(sub[:, 1] % 8 == x)
         cost = np.array([spans[i[4]:i[4] + i[5], 2].sum() for i in sub])
-        assert np.all(np.diff(cost) <= 0)
+        if not key_major:
+            assert np.all(np.diff(cost) <= 0)
+            continue
+        assert np.all(np.diff(sub[:, 1]) >= 0)
+        for h in np.unique(sub[:, 1]):
+            assert np.all(np.diff(cost[sub[:, 1] == h]) <= 0)
 
 
 def test_token_masks_that_split_frames_run_on_the_compacted_stream():
