@@ -19,6 +19,7 @@ constexpr int kDkvQueryStep = 32;
 
 constexpr int kThreads = 256;  // block size of the element-wise kernels (delta, fill, gather, scatter)
 constexpr int kNumXcd = 8;  // MI355X: 8 accelerator complex dies; workgroups go round-robin
+constexpr int kCusPerXcd = 32;  // 256 compute units
 
 // One work item: a tile of rows of one stream and head, and the list of row ranges of the
 // other side it pairs with (key spans for query tiles, query spans for key tiles).

@@ -5,6 +5,7 @@ into per-pair coverage counts; each must equal the oracle's 0/1 mask exactly: ev
 visible pair computed once, nothing else computed. Pair counts are checked against the
 closed form and the golden values the oracle wrote.
 """
+import heapq
 import json
 import os
 
@@ -222,3 +223,36 @@ def test_key_tiles_cross_reference_groups_with_key_ranges():
                 ranged.append((it[2] + lo, it[2] + hi))
     assert sorted(ranged) == [(0, 100), (100, 200), (200, 256), (256, 300), (300, 400), (400, 500)]
     assert sra.schedule_info(samples, sra.SCHED_BWD_DKDV)[2] == sum(sra.pair_counts(samples))
+
+
+def test_key_tile_phases_rotate_the_gen_span_and_keep_every_pair():
+    """With heads pinned to XCDs, each dK/dV key tile starts its gen query span at the step
+    that its compute unit is predicted to reach it (the XCD's launch order replayed on 32
+    compute units, one resident tile each, time in 32-row steps), and wraps around: the span is
+    cut in two and the tile's other spans are unchanged."""
+    samples = [SampleGeom(4, 48, 48, 3, 48, 48)]  # 36 gen + 27 ref key tiles per head
+    g = samples[0]
+    aligned, a_spans = sra.schedule_export(samples, sra.SCHED_BWD_DKDV, heads=8)
+    plain, p_spans = sra.schedule_export(samples, sra.SCHED_BWD_DKDV, heads=1)  # 1 % 8: no phases
+    canon = {(int(i[0]), int(i[2]), int(i[3])): p_spans[i[4]:i[4] + i[5]] for i in plain}
+    steps = -(-g.n_gen // 32)
+    rotated = 0
+    for x in range(8):
+        free = [0] * 32
+        for it in aligned[x::8]:
+            if it[0] < 0:
+                continue
+            own = a_spans[it[4]:it[4] + it[5]]
+            ref = canon[(int(it[0]), int(it[2]), int(it[3]))]
+            t0 = heapq.heappop(free)
+            heapq.heappush(free, t0 + int(sum(-(-int(s[2]) // 32) for s in own)))
+            phase = (t0 % steps) * 32
+            if phase == 0:
+                assert np.array_equal(own, ref)
+                continue
+            rotated += 1
+            assert it[5] == len(ref) + 1
+            assert tuple(own[0]) == (0, phase, g.n_gen - phase, 0)
+            assert tuple(own[1]) == (0, 0, phase, 0)
+            assert np.array_equal(own[2:], ref[1:])
+    assert rotated > 8 * 20
