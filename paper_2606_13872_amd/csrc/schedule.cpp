@@ -253,6 +253,55 @@ void order_items(std::vector<std::pair<int64_t, WorkItem>>& v, int32_t heads, bo
     for (int x = 0; x < kNumXcd; ++x) s->items.push_back(j < per[x].size() ? per[x][j] : pad);
 }
 
+// Phase alignment of a schedule (runs after order_items with heads pinned to XCDs). The first
+// span of a key tile is the sample's gen query rows, and that of a gen query tile the sample's
+// gen keys: every such tile of a sample and head streams the same rows, and the tiles resident
+// on an XCD share them through its L2 only while they are at nearby steps of the span at the
+// same time. Tiles start whenever a compute unit frees up, so tiles of different lengths drift
+// apart. Here each XCD's launch order is replayed on its compute units (one resident tile
+// each, time counted in steps of the inner loop): a tile predicted to start at time t begins
+// its first span at step t mod S (S = the span's steps) and wraps around, so that all tiles
+// stream step t mod S at time t. The tile's pairs are unchanged (the span is cut in two); only
+// the order of the sums changes, fixed by the plan.
+void align_phases(int step, Schedule* s) {
+  std::vector<Span> spans;
+  std::map<std::pair<int32_t, int32_t>, int32_t> made;  // (span list, phase in rows) -> offset
+  const size_t n = s->items.size();
+  for (int x = 0; x < kNumXcd; ++x) {
+    std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> free_at;
+    for (int c = 0; c < kCusPerXcd; ++c) free_at.push(0);
+    for (size_t k = size_t(x); k < n; k += kNumXcd) {
+      WorkItem& w = s->items[k];
+      if (w.stream < 0) continue;
+      const Span* l = &s->spans[size_t(w.span_off)];
+      int64_t cost = 0;
+      for (int32_t i = 0; i < w.span_cnt; ++i) cost += (l[i].len + step - 1) / step;
+      const int64_t t0 = free_at.top();
+      free_at.pop();
+      free_at.push(t0 + cost);
+      const int64_t first_steps = (l[0].len + step - 1) / step;
+      int32_t phase = 0;
+      if (l[0].stream == 0 && l[0].keys == 0 && first_steps > 1) phase = int32_t(t0 % first_steps) * step;
+      const auto key = std::make_pair(w.span_off, phase);
+      auto it = made.find(key);
+      if (it == made.end()) {
+        const int32_t off = int32_t(spans.size());
+        if (phase == 0) {
+          spans.push_back(l[0]);
+        } else {
+          spans.push_back({l[0].stream, l[0].start + phase, l[0].len - phase, 0});
+          spans.push_back({l[0].stream, l[0].start, phase, 0});
+        }
+        spans.insert(spans.end(), l + 1, l + w.span_cnt);
+        it = made.emplace(key, off).first;
+      }
+      w.span_cnt += phase == 0 ? 0 : 1;
+      w.span_off = it->second;
+    }
+  }
+  s->spans.swap(spans);
+}
+
 // Query-major schedule (forward and dQ): query tiles of `tile` rows, key spans per class.
 void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
   std::vector<TileClass> classes;
@@ -294,6 +343,7 @@ void build_query_major(const Layout& L, int tile, int step, Schedule* s) {
   std::vector<std::pair<int64_t, WorkItem>> v;
   for (const TileClass& c : classes) emit_items(c, tile, L.heads, step, s->spans, &v);
   order_items(v, L.heads, false, s);
+  if (L.heads % kNumXcd == 0) align_phases(step, s);
 }
 
 // First frame of the ref group holding sample-relative ref row r.
@@ -303,54 +353,6 @@ int32_t group_of_row(const SampleLayout& s, int64_t r) {
     return int32_t(it - s.gbound.begin() - 1) * s.group;
   }
   return int32_t(r / s.F) / s.group * s.group;
-}
-
-// Phase alignment of a key-major schedule (runs after order_items with heads pinned to XCDs).
-// A key tile's first span is the sample's gen query rows, which every key tile of that sample
-// and head streams; the tiles resident on an XCD share those rows through its L2 only while
-// they are at nearby steps of the span at the same time. Tiles start whenever a compute unit
-// frees up, so tiles of different lengths drift apart. Here each XCD's launch order is
-// replayed on its compute units (one resident tile each, time counted in query steps): a tile
-// predicted to start at time t begins its first span at step t mod S (S = the span's steps)
-// and wraps around, so that all tiles stream step t mod S at time t. The tile's pairs are
-// unchanged (the span is cut in two); only the order of the sums changes, fixed by the plan.
-void align_phases(int step, Schedule* s) {
-  std::vector<Span> spans;
-  std::map<std::pair<int32_t, int32_t>, int32_t> made;  // (span list, phase in rows) -> offset
-  const size_t n = s->items.size();
-  for (int x = 0; x < kNumXcd; ++x) {
-    std::priority_queue<int64_t, std::vector<int64_t>, std::greater<int64_t>> free_at;
-    for (int c = 0; c < kCusPerXcd; ++c) free_at.push(0);
-    for (size_t k = size_t(x); k < n; k += kNumXcd) {
-      WorkItem& w = s->items[k];
-      if (w.stream < 0) continue;
-      const Span* l = &s->spans[size_t(w.span_off)];
-      int64_t cost = 0;
-      for (int32_t i = 0; i < w.span_cnt; ++i) cost += (l[i].len + step - 1) / step;
-      const int64_t t0 = free_at.top();
-      free_at.pop();
-      free_at.push(t0 + cost);
-      const int64_t first_steps = (l[0].len + step - 1) / step;
-      int32_t phase = 0;
-      if (l[0].stream == 0 && l[0].keys == 0 && first_steps > 1) phase = int32_t(t0 % first_steps) * step;
-      const auto key = std::make_pair(w.span_off, phase);
-      auto it = made.find(key);
-      if (it == made.end()) {
-        const int32_t off = int32_t(spans.size());
-        if (phase == 0) {
-          spans.push_back(l[0]);
-        } else {
-          spans.push_back({l[0].stream, l[0].start + phase, l[0].len - phase, 0});
-          spans.push_back({l[0].stream, l[0].start, phase, 0});
-        }
-        spans.insert(spans.end(), l + 1, l + w.span_cnt);
-        it = made.emplace(key, off).first;
-      }
-      w.span_cnt += phase == 0 ? 0 : 1;
-      w.span_off = it->second;
-    }
-  }
-  s->spans.swap(spans);
 }
 
 // Key-major schedule (dK/dV): key tiles, query spans per class.

@@ -225,17 +225,19 @@ def test_key_tiles_cross_reference_groups_with_key_ranges():
     assert sra.schedule_info(samples, sra.SCHED_BWD_DKDV)[2] == sum(sra.pair_counts(samples))
 
 
-def test_key_tile_phases_rotate_the_gen_span_and_keep_every_pair():
-    """With heads pinned to XCDs, each dK/dV key tile starts its gen query span at the step
-    that its compute unit is predicted to reach it (the XCD's launch order replayed on 32
-    compute units, one resident tile each, time in 32-row steps), and wraps around: the span is
-    cut in two and the tile's other spans are unchanged."""
-    samples = [SampleGeom(4, 48, 48, 3, 48, 48)]  # 36 gen + 27 ref key tiles per head
+@pytest.mark.parametrize("which,step", [(0, 64), (1, 32), (2, 32)])
+def test_tile_phases_rotate_the_gen_span_and_keep_every_pair(which, step):
+    """With heads pinned to XCDs, each tile whose first span is the sample's gen rows (dK/dV key
+    tiles: gen queries; forward and dQ gen query tiles: gen keys) starts that span at the step
+    its compute unit is predicted to reach (the XCD's launch order replayed on 32 compute
+    units, one resident tile each, time in inner steps), and wraps around: the span is cut in
+    two and the tile's other spans are unchanged."""
+    samples = [SampleGeom(4, 48, 48, 3, 48, 48)]  # 36 gen + 27 ref tiles per head
     g = samples[0]
-    aligned, a_spans = sra.schedule_export(samples, sra.SCHED_BWD_DKDV, heads=8)
-    plain, p_spans = sra.schedule_export(samples, sra.SCHED_BWD_DKDV, heads=1)  # 1 % 8: no phases
+    aligned, a_spans = sra.schedule_export(samples, which, heads=8)
+    plain, p_spans = sra.schedule_export(samples, which, heads=1)  # 1 % 8: no phases
     canon = {(int(i[0]), int(i[2]), int(i[3])): p_spans[i[4]:i[4] + i[5]] for i in plain}
-    steps = -(-g.n_gen // 32)
+    steps = -(-g.n_gen // step)
     rotated = 0
     for x in range(8):
         free = [0] * 32
@@ -245,8 +247,8 @@ def test_key_tile_phases_rotate_the_gen_span_and_keep_every_pair():
             own = a_spans[it[4]:it[4] + it[5]]
             ref = canon[(int(it[0]), int(it[2]), int(it[3]))]
             t0 = heapq.heappop(free)
-            heapq.heappush(free, t0 + int(sum(-(-int(s[2]) // 32) for s in own)))
-            phase = (t0 % steps) * 32
+            heapq.heappush(free, t0 + int(sum(-(-int(s[2]) // step) for s in own)))
+            phase = (t0 % steps) * step if ref[0][0] == 0 else 0
             if phase == 0:
                 assert np.array_equal(own, ref)
                 continue
@@ -255,4 +257,4 @@ def test_key_tile_phases_rotate_the_gen_span_and_keep_every_pair():
             assert tuple(own[0]) == (0, phase, g.n_gen - phase, 0)
             assert tuple(own[1]) == (0, 0, phase, 0)
             assert np.array_equal(own[2:], ref[1:])
-    assert rotated > 8 * 20
+    assert rotated >= 8 * 4  # every tile past the first 32 of each XCD starts late
