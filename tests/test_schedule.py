@@ -115,7 +115,7 @@ def test_full_size_pair_counts_and_coverage(name):
         assert covered == gp + rp
 
 
-def test_survey_quoted_pair_counts():
+def test_hand_derived_pair_counts():
     """Hand-derived closed forms G(G+R) + R F for the named workloads."""
     g = _golden()
     assert g["tiny"]["gen_pairs"] + g["tiny"]["ref_pairs"] == 128 * 384 + 256 * 64 == 65536
