@@ -163,12 +163,28 @@ class Problem:
         return ctypes.byref(self.c)
 
     def workspace_size(self, backward: bool) -> int:
-        n = ctypes.c_size_t(0)
-        _check(lib().sra_workspace_size(self.ptr, 1 if backward else 0, ctypes.byref(n)))
-        return int(n.value)
+        """Bytes of workspace one call needs (fixed by the geometry, so asked once per direction)."""
+        cache = self.__dict__.setdefault("_ws", {})
+        b = bool(backward)
+        if b not in cache:
+            n = ctypes.c_size_t(0)
+            _check(lib().sra_workspace_size(self.ptr, 1 if b else 0, ctypes.byref(n)))
+            cache[b] = int(n.value)
+        return cache[b]
 
 
 _PROBLEMS: "OrderedDict" = None
+
+
+_FROZEN_TYPES: Dict[type, bool] = {}
+
+
+def _frozen_type(cls) -> bool:
+    """Whether instances of cls are frozen dataclasses (immutable, so usable as a cache key)."""
+    f = _FROZEN_TYPES.get(cls)
+    if f is None:
+        f = _FROZEN_TYPES[cls] = bool(getattr(getattr(cls, "__dataclass_params__", None), "frozen", False))
+    return f
 
 
 def _problem(samples, heads, head_dim, scale, gen_stride, ref_stride, flags) -> Problem:
@@ -179,7 +195,7 @@ def _problem(samples, heads, head_dim, scale, gen_stride, ref_stride, flags) -> 
 
     if _PROBLEMS is None:
         _PROBLEMS = OrderedDict()
-    frozen = all(getattr(getattr(g, "__dataclass_params__", None), "frozen", False) for g in samples)
+    frozen = all(_frozen_type(type(g)) for g in samples)
     try:
         if not frozen:  # geometry objects that may change between calls are never cached
             raise TypeError
@@ -271,8 +287,11 @@ def kernel_timing() -> Dict[str, Tuple[float, int]]:
 
 # ----------------------------------------------------------------------------- device calls
 def _stream_ptr(device):
-    import torch
-
+    """The current HIP stream of `device` (torch's, as a raw pointer)."""
+    torch = _tm()
+    raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    if raw is not None:
+        return ctypes.c_void_p(raw(device.index))
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
@@ -285,11 +304,12 @@ def _token_stride(ts, name):
     for t in ts:
         if t is None or t.numel() == 0:
             continue
-        if t.dim() != 3 or t.stride(2) != 1 or t.stride(1) != t.shape[2]:
+        st = t.stride()
+        if len(st) != 3 or st[2] != 1 or st[1] != t.shape[2]:
             raise ValueError(f"{name}: tensors must be [tokens, heads, head_dim] with contiguous heads")
         if s0 is None:
-            s0 = t.stride(0)
-        elif t.stride(0) != s0:
+            s0 = st[0]
+        elif st[0] != s0:
             raise ValueError(f"{name}: q, k and v must share one token stride")
     return 0 if s0 is None else int(s0)
 
@@ -346,8 +366,10 @@ def _expect(t, name, shape, dtype, dense):
     if dense:
         if not t.is_contiguous():
             raise _bad(f"{name} must be dense (contiguous)")
-    elif t.numel() and (t.stride(2) != 1 or (shape[1] > 1 and t.stride(1) != shape[2])):
-        raise _bad(f"{name} must be [tokens, heads, head_dim] with contiguous heads")
+    elif t.numel():
+        st = t.stride()
+        if st[2] != 1 or (shape[1] > 1 and st[1] != shape[2]):
+            raise _bad(f"{name} must be [tokens, heads, head_dim] with contiguous heads")
 
 
 def _same_device(tensors, device):
@@ -381,12 +403,12 @@ def _inputs(q_gen, k_gen, v_gen, q_ref, k_ref, v_ref, samples, gen_only):
 
 
 def _out(out, name, shape, dtype, device):
-    """The caller's output buffer `name` (checked: dtype, shape, dense, device), or a new one
-    (allocated only when none was given)."""
+    """The caller's output buffer `name`, or a new one (allocated only when none was given).
+    dtype, shape and layout of a given buffer were checked by _precheck_outs; its device is
+    checked here."""
     t = out.get(name)
     if t is None:
         return _tm().empty(shape, dtype=dtype, device=device)
-    _expect(t, name, shape, dtype, True)
     _same_device(((name, t),), device)
     return t
 
