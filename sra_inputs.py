@@ -116,6 +116,10 @@ def workload(name: str) -> Workload:
         return Workload(name, [SampleGeom(21, 30, 52, n, 30, 52)], 40, 128, 2, True)
     if name == "720p":
         return Workload(name, [SampleGeom(21, 45, 80, 21, 45, 80)], 40, 128, 3, False)
+    if name == "720p_whole_ref":
+        # the 720p layer with one self-attention group over the whole reference (g = T_r): the
+        # other reading of the reference groups, which the reference K/V cache also keeps linear
+        return Workload(name, [SampleGeom(21, 45, 80, 21, 45, 80, group_frames=21)], 40, 128, 8, False)
     if name == "varlen":
         return Workload(name, [SampleGeom(5, 68, 120, r, 68, 120) for r in VARLEN_REF_FRAMES],
                         24, 128, 4, True)

@@ -90,7 +90,8 @@ def _close(name, got, want):
     assert rel <= REL, f"{name}: relative err {rel:.3e}"
 
 
-@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "varlen", "varlen_window", "varlen_tokens"])
+@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "720p_whole_ref", "varlen", "varlen_window",
+                                  "varlen_tokens"])
 def test_fullsize_forward_sampled_rows(name):
     w = workload(name)
     x = _inputs(w, grads=False)
@@ -114,7 +115,7 @@ def test_fullsize_forward_sampled_rows(name):
             assert err <= LSE_ABS, f"{name} LSE h{h} b{b}: {err:.3e}"
 
 
-@pytest.mark.parametrize("name", ["720p", "varlen"])
+@pytest.mark.parametrize("name", ["720p", "720p_whole_ref", "varlen"])
 def test_fullsize_dq_sampled_rows(name):
     w = workload(name)
     x = _inputs(w, grads=True)
@@ -157,12 +158,15 @@ def _keys_720p(geom, rng):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("name,h", [("varlen_tokens", 1), ("varlen_window", 1), ("720p", 0), ("720p", 39)])
+@pytest.mark.parametrize("name,h", [("varlen_tokens", 1), ("varlen_window", 1), ("720p", 0), ("720p", 39),
+                                    ("720p_whole_ref", 0)])
 def test_fullsize_dkv_sampled_keys(name, h):
     """dK/dV of sampled keys against the oracle's sums over every query that sees each key (the
     sample with the shortest reference, one head). The oracle runs every query row that sees a
     sampled key through its full masked softmax: about 10 s per varlen case and 40 s per 720p
-    head (75,600 gen rows x 151,200 keys, fp32, in blocks of 2,048 rows) on 16 host threads."""
+    head (75,600 gen rows x 151,200 keys, fp32, in blocks of 2,048 rows) on 16 host threads,
+    about 60 s with the whole reference as one group (every reference row sees every reference
+    key)."""
     w = workload(name)
     x = _inputs(w, grads=True)
     ins = [x[k] for k in INS]
@@ -172,7 +176,7 @@ def test_fullsize_dkv_sampled_keys(name, h):
     go, ro = _offsets(w.samples)
     b = int(np.argmin([s.n_ref for s in w.samples]))
     geom = w.samples[b]
-    big = name == "720p"
+    big = name.startswith("720p")
     keys = _keys_720p(geom, np.random.default_rng(9)) if big else _sample_keys(geom, np.random.default_rng(9))
     xh = _head_view(x, h)
     print(f"[fullsize] {name} dK/dV head {h} sample {b}: {len(keys)} keys", flush=True)
@@ -199,7 +203,8 @@ def _ref_token_ok(geom):
     return ok
 
 
-@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "varlen", "varlen_window", "varlen_tokens"])
+@pytest.mark.parametrize("name", ["480p", "sweep_256", "720p", "720p_whole_ref", "varlen", "varlen_window",
+                                  "varlen_tokens"])
 def test_fullsize_zero_keys_count_law(name):
     """K = 0 makes every visible logit 0, so LSE = ln(number of visible keys) for every row
     (and -inf for rows of invalid reference tokens)."""
@@ -232,7 +237,7 @@ def test_fullsize_zero_keys_count_law(name):
 IDENTITY_REL = 0.04
 
 
-@pytest.mark.parametrize("name", ["720p", "varlen", "sweep_256", "varlen_tokens"])
+@pytest.mark.parametrize("name", ["720p", "720p_whole_ref", "varlen", "sweep_256", "varlen_tokens"])
 def test_fullsize_gradient_identities(name):
     """Per sample, head and dim: sum_k dK_k = 0 (each query's dS row sums to 0) and
     sum_k dV_k = sum_q dO_q over valid queries (each query's P row sums to 1), to within

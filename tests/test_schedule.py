@@ -258,3 +258,15 @@ def test_tile_phases_rotate_the_gen_span_and_keep_every_pair(which, step):
             assert tuple(own[1]) == (0, 0, phase, 0)
             assert np.array_equal(own[2:], ref[1:])
     assert rotated >= 8 * 4  # every tile past the first 32 of each XCD starts late
+
+
+def test_whole_reference_group_pair_counts():
+    """With one self-attention group over the whole reference (g = T_r), every valid reference
+    query sees every valid reference key: G (G + R) + R^2 pairs per head, and every schedule
+    covers exactly those."""
+    w = workload("720p_whole_ref")
+    g = w.samples[0]
+    G, R = g.n_gen, g.n_ref
+    assert sra.pair_counts(w.samples, w.heads, w.head_dim) == (G * (G + R), R * R)
+    for which in SCHEDS:
+        assert sra.schedule_info(w.samples, which, w.heads, w.head_dim)[2] == G * (G + R) + R * R
