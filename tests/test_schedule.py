@@ -270,3 +270,30 @@ def test_whole_reference_group_pair_counts():
     assert sra.pair_counts(w.samples, w.heads, w.head_dim) == (G * (G + R), R * R)
     for which in SCHEDS:
         assert sra.schedule_info(w.samples, which, w.heads, w.head_dim)[2] == G * (G + R) + R * R
+
+
+def _random_geom(rng):
+    """A sample big enough that head 0 alone has more work items than one XCD has compute
+    units, so the phases of the pinned order come into play."""
+    gf, gh, gw = int(rng.integers(3, 6)), int(rng.integers(30, 49)), int(rng.integers(40, 57))
+    rf = int(rng.integers(2, 7))
+    g = int(rng.integers(1, 4))
+    fv = tuple(int(v) for v in (rng.random(rf) >= 0.25)) if rng.random() < 0.5 else None
+    win = int(rng.integers(0, 3)) if rng.random() < 0.4 else None
+    return SampleGeom(gf, gh, gw, rf, gh, gw, group_frames=g, frame_valid=fv, gen_window=win)
+
+
+@pytest.mark.parametrize("seed", range(4))
+@pytest.mark.parametrize("which", SCHEDS)
+def test_random_pinned_schedules_cover_the_mask(seed, which):
+    """Random geometries (groups, invalid frames, windows) with 8 heads, so that heads are
+    pinned to XCDs and the phases rotate spans: head 0's schedule still covers exactly the
+    oracle's mask, and the covered pair count over all heads equals the closed form."""
+    rng = np.random.default_rng(100 + seed)
+    samples = [_random_geom(rng)]
+    items, _ = sra.schedule_export(samples, which, heads=8)
+    assert (items[:, 0] >= 0).sum() > 8 * 32
+    want = oracle.visibility_mask(samples[0]).astype(np.uint8)
+    got = sra.schedule_mask(samples, which, 0, heads=8)
+    assert np.array_equal(got, want), np.argwhere(got != want)[:5]
+    assert sra.schedule_info(samples, which, heads=8)[2] == sum(sra.pair_counts(samples))
