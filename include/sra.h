@@ -211,6 +211,11 @@ sra_status sra_schedule_mask(const sra_problem* p, int which, int32_t sample, ui
  * the dK/dV schedule only: the item's keys [lo, hi), counted from its first key, that the
  * span's queries see, packed lo | hi << 16, or 0 for all of them).
  * items/spans may be NULL to query only; capacities count int32 elements.
+ * Items are listed in launch order (item i runs on XCD i % 8). When the head count is a
+ * multiple of 8, an item whose first span is its sample's gen rows may start that span part
+ * way in and wrap around (the span then appears as two entries, its tail first), so that the
+ * items resident on one XCD stream the same rows at the same time; the rows covered are the
+ * same either way.
  * When token masks split reference frames into more runs of valid tokens than there are
  * groups with a valid token, the library runs on the compacted reference stream (the valid
  * reference tokens of the batch back to back, in sample, group and token order: gathered
