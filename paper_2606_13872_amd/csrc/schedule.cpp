@@ -272,7 +272,7 @@ void align_phases(int step, Schedule* s) {
     for (int c = 0; c < kCusPerXcd; ++c) free_at.push(0);
     for (size_t k = size_t(x); k < n; k += kNumXcd) {
       WorkItem& w = s->items[k];
-      if (w.stream < 0) continue;
+      if (w.stream < 0 || w.span_cnt <= 0) continue;
       const Span* l = &s->spans[size_t(w.span_off)];
       int64_t cost = 0;
       for (int32_t i = 0; i < w.span_cnt; ++i) cost += (l[i].len + step - 1) / step;
